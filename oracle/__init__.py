@@ -1,0 +1,154 @@
+"""CPU oracle for the ShiftAddLLM shift-add linear layer (fp64).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(``paper_2406_05981_amd``) never imports it and shares no code with it.
+
+The arithmetic lives in ``oracle.c`` (plain fp64 C, OpenMP over outputs); this
+module only builds and loads it and marshals numpy arrays.  What each function
+computes, with the passage it follows:
+
+* :func:`pack` / :func:`unpack` -- the 8-bit keys of Sec. 4.1 ("every eight
+  grouped binary weights form an 8-bit key"): byte c of a plane row is
+  ``sum_j [s[8c+j] > 0] << j``; bit value 1 stands for +1 (a reading: the paper
+  does not fix the bit order or the bit-to-sign map).
+* :func:`lut` -- the 256 precomputed partial sums per 8 activations of Sec. 4.1:
+  ``lut[b][c][m] = sum_j (2 bit_j(m) - 1) x[b][8c+j]``.
+* :func:`shiftadd_gemm` -- the layer ``y = x W_q^T`` with
+  ``W_q = sum_i 2^{e_i} b_i`` (Sec. 3 BCQ with the power-of-two factors of
+  Eq. 2, one factor per plane, row and group of G columns), and the sum of the
+  magnitudes of its terms (the tolerance reference).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` with gcc into ``liboracle.so`` next to it."""
+    if not force and os.path.exists(_LIB_PATH) and \
+            os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
+        return _LIB_PATH
+    tmp = _LIB_PATH + f".tmp{os.getpid()}"
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Wextra",
+           "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build(force=False)
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    lib.oracle_max_threads.argtypes = [ctypes.c_int]
+    lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_pack.argtypes = [P, I64, I64, I64, P]
+    lib.oracle_pack.restype = None
+    lib.oracle_unpack.argtypes = [P, I64, I64, I64, P]
+    lib.oracle_unpack.restype = None
+    lib.oracle_lut.argtypes = [P, I64, I64, P]
+    lib.oracle_lut.restype = None
+    lib.oracle_shiftadd_gemm.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, P, ctypes.c_int]
+    lib.oracle_shiftadd_gemm.restype = None
+    lib.oracle_shiftadd_gemm_rows.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64,
+                                              P, P, ctypes.c_int]
+    lib.oracle_shiftadd_gemm_rows.restype = None
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _check_shapes(signs: np.ndarray, exps: np.ndarray, x: np.ndarray, G: int):
+    q, N, K = signs.shape
+    B = x.shape[0]
+    if K % 8 or G % 8 or K % G:
+        raise ValueError(f"need K % 8 == 0, G % 8 == 0, K % G == 0 (K={K}, G={G})")
+    if exps.shape != (q, N, K // G):
+        raise ValueError(f"exps shape {exps.shape} != {(q, N, K // G)}")
+    if x.shape != (B, K):
+        raise ValueError(f"x shape {x.shape} != {(B, K)}")
+    return q, N, K, B
+
+
+def max_threads(nthreads: int = 0) -> int:
+    return int(_load().oracle_max_threads(int(nthreads)))
+
+
+def pack(signs: np.ndarray) -> np.ndarray:
+    """Canonical packed planes ``uint8 [q][N][K/8]`` of ``int8 [q][N][K]`` signs."""
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    q, N, K = signs.shape
+    if K % 8:
+        raise ValueError("K must be a multiple of 8")
+    out = np.empty((q, N, K // 8), dtype=np.uint8)
+    _load().oracle_pack(_ptr(signs), q, N, K, _ptr(out))
+    return out
+
+
+def unpack(packed: np.ndarray, K: int) -> np.ndarray:
+    """Inverse of :func:`pack`: ``int8 [q][N][K]`` in {-1, +1}."""
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    q, N, C = packed.shape
+    if C * 8 != K:
+        raise ValueError("packed.shape[2] * 8 must equal K")
+    out = np.empty((q, N, K), dtype=np.int8)
+    _load().oracle_unpack(_ptr(packed), q, N, K, _ptr(out))
+    return out
+
+
+def lut(x: np.ndarray) -> np.ndarray:
+    """Tables ``fp64 [B][K/8][256]`` of the activations ``x [B][K]`` (fp16 or wider)."""
+    x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
+    B, K = x64.shape
+    if K % 8:
+        raise ValueError("K must be a multiple of 8")
+    out = np.empty((B, K // 8, 256), dtype=np.float64)
+    _load().oracle_lut(_ptr(x64), B, K, _ptr(out))
+    return out
+
+
+def shiftadd_gemm(x: np.ndarray, signs: np.ndarray, exps: np.ndarray, G: int,
+                  nthreads: int = 0, rows: Optional[Sequence[int]] = None
+                  ) -> Tuple[np.ndarray, np.ndarray]:
+    """``(y, absterm)``, both fp64 ``[B][N]`` (or ``[B][len(rows)]``).
+
+    ``y[b][n] = sum_i sum_g ldexp(sum_{k in g} s_i[n][k] x[b][k], e[i][n][g])`` and
+    ``absterm[b][n] = sum_i sum_k 2^e |x[b][k]|``.
+    """
+    x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    exps = np.ascontiguousarray(exps, dtype=np.int8)
+    q, N, K, B = _check_shapes(signs, exps, x64, G)
+    lib = _load()
+    if rows is None:
+        y = np.empty((B, N), dtype=np.float64)
+        a = np.empty((B, N), dtype=np.float64)
+        lib.oracle_shiftadd_gemm(_ptr(x64), _ptr(signs), _ptr(exps), q, N, K, G, B,
+                                 _ptr(y), _ptr(a), int(nthreads))
+    else:
+        r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        if r.size and (r.min() < 0 or r.max() >= N):
+            raise ValueError("row index out of range")
+        y = np.empty((B, r.size), dtype=np.float64)
+        a = np.empty((B, r.size), dtype=np.float64)
+        lib.oracle_shiftadd_gemm_rows(_ptr(x64), _ptr(signs), _ptr(exps), q, N, K, G, B,
+                                      _ptr(r), r.size, _ptr(y), _ptr(a), int(nthreads))
+    return y, a

@@ -1,0 +1,179 @@
+"""Seeded synthetic inputs for the shift-add linear layer.
+
+This module is shared by the CPU oracle (tests, cpu baseline) and the GPU path
+(tests, bench).  It only draws random numbers: it holds none of the method's
+arithmetic (no bit packing, no table construction, no scaling).
+
+What is drawn, per layer of shape N x K with q binary planes and group size G
+(ShiftAddLLM, Sec. 3 "Binary-coding Quantization" and Sec. 4.1):
+
+* ``signs``  int8 ``[q][N][K]`` in {-1, +1}: the binary matrices b_i, each entry
+  an independent fair coin (the Bernoulli(0.5) planes of the synthetic layers).
+* ``exps``   int8 ``[q][N][K/G]``: the power-of-two exponents P of the scaling
+  factors 2^P (Eq. 2), uniform over an inclusive integer range.  The sign of a
+  scaling factor is assumed folded into the plane, so only magnitudes remain.
+* ``x``      fp16 ``[B][K]``: activations N(0, 1); for the workloads with
+  outliers, round(0.01 K) channels (the same for every batch row, drawn without
+  replacement) are multiplied by 20 before the cast to fp16.
+
+Draw order per layer is fixed: signs, exps, x, outlier channels, from
+``numpy.random.default_rng(SeedSequence([seed, config_id, layer_id]))``.
+
+The paper's own evaluation data (WikiText-2, zero-shot suites, pretrained
+OPT/LLaMA weights) is not available; these layers reproduce only the shapes,
+bit widths and group sizes of the paper's OPT/LLaMA projections.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "Layer",
+    "Workload",
+    "WORKLOADS",
+    "workload",
+    "layer_inputs",
+    "random_case",
+    "mixed_bits",
+    "sha256",
+]
+
+
+@dataclasses.dataclass(frozen=True)
+class Layer:
+    name: str
+    N: int  # output rows
+    K: int  # input columns (reduction dimension)
+    q: int  # binary planes
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    key: str
+    config_id: int
+    description: str
+    layers: Tuple[Layer, ...]
+    group: int
+    exp_range: Tuple[int, int]  # inclusive
+    outlier_fraction: float  # fraction of channels scaled by outlier_scale
+    outlier_scale: float
+    batches: Tuple[int, ...]
+    depth: int = 1  # decoder depth the layer set is replicated over
+
+
+def mixed_bits(seed: int = 0, n_layers: int = 7, choices=(2, 3, 4), mean: int = 3) -> List[int]:
+    """Per-layer bit widths for the mixed-precision 7B layer set.
+
+    Draw n_layers values uniformly from ``choices`` and redraw until their mean
+    over layers equals ``mean`` (the budget of Eq. 4 counts layers, not
+    parameters).
+    """
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 4, 999]))
+    target = mean * n_layers
+    while True:
+        qs = [int(v) for v in rng.choice(np.asarray(choices), size=n_layers)]
+        if sum(qs) == target:
+            return qs
+
+
+def _layer_set(seed: int = 0) -> Tuple[Layer, ...]:
+    names = ["q_proj", "k_proj", "v_proj", "o_proj", "up_proj", "gate_proj", "down_proj"]
+    shapes = [(4096, 4096)] * 4 + [(11008, 4096)] * 2 + [(4096, 11008)]
+    qs = mixed_bits(seed)
+    return tuple(Layer(n, N, K, q) for n, (N, K), q in zip(names, shapes, qs))
+
+
+WORKLOADS: Dict[str, Workload] = {
+    w.key: w
+    for w in (
+        Workload(
+            "opt125m_proj", 0,
+            "OPT-125M-shaped projection 768x768, q=3, G=128, exps in [-8,-2], x ~ N(0,1)",
+            (Layer("proj", 768, 768, 3),), 128, (-8, -2), 0.0, 1.0, (1,)),
+        Workload(
+            "llama2_7b_attn", 1,
+            "LLaMA-2-7B attention projection 4096x4096, q=3, G=128, exps in [-10,-3], "
+            "x ~ N(0,1) with 1% of channels x20",
+            (Layer("attn_proj", 4096, 4096, 3),), 128, (-10, -3), 0.01, 20.0, (1,)),
+        Workload(
+            "llama2_7b_mlp_q2", 2,
+            "LLaMA-2-7B MLP pair at q=2: up/gate 11008x4096 and down 4096x11008, G=128, "
+            "exps in [-10,-3], x ~ N(0,1)",
+            (Layer("up_gate", 11008, 4096, 2), Layer("down", 4096, 11008, 2)),
+            128, (-10, -3), 0.0, 1.0, (1, 4, 16)),
+        Workload(
+            "llama2_70b_mlp", 3,
+            "LLaMA-2-70B-shaped MLP: 28672x8192 and 8192x28672, q=3, G=128, exps in [-12,-3], "
+            "x ~ N(0,1)",
+            (Layer("up", 28672, 8192, 3), Layer("down", 8192, 28672, 3)),
+            128, (-12, -3), 0.0, 1.0, (1, 8)),
+        Workload(
+            "llama2_7b_layer_set", 4,
+            "LLaMA-2-7B decoder linear layers (q,k,v,o 4096x4096; up, gate 11008x4096; "
+            "down 4096x11008) with per-layer q in {2,3,4}, mean 3 over layers, G=128, "
+            "exps in [-10,-3], x ~ N(0,1) with 1% of channels x20, replicated over 32 layers",
+            _layer_set(0), 128, (-10, -3), 0.01, 20.0, (1, 4, 8, 16), depth=32),
+    )
+}
+
+
+def workload(key: str) -> Workload:
+    return WORKLOADS[key]
+
+
+def sha256(a: np.ndarray) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def _draw(rng: np.random.Generator, q: int, N: int, K: int, G: int, B: int,
+          exp_range: Tuple[int, int], outlier_fraction: float, outlier_scale: float):
+    # signs: fair coins mapped to {-1, +1}
+    signs = rng.integers(0, 2, size=(q, N, K), dtype=np.int8)
+    signs *= 2
+    signs -= 1
+    exps = rng.integers(exp_range[0], exp_range[1] + 1, size=(q, N, K // G), dtype=np.int8)
+    x = rng.standard_normal((B, K))
+    n_out = int(round(outlier_fraction * K))
+    idx = np.zeros(0, dtype=np.int64)
+    if n_out > 0:
+        idx = rng.choice(K, size=n_out, replace=False)
+        x[:, idx] *= outlier_scale
+    x16 = x.astype(np.float16)
+    return signs, exps, x16, np.sort(idx)
+
+
+def layer_inputs(key: str, layer: int, batch: int, seed: int = 0, copy: int = 0) -> dict:
+    """Inputs of one layer of a named workload.
+
+    ``copy`` selects a distinct replica of the layer (another decoder depth in the
+    layer set, or another weight copy that benchmarks rotate through so that the
+    last-level cache cannot serve the weights).  Weights do not depend on
+    ``batch``: the same seed gives the same planes and exponents at every batch.
+    """
+    w = WORKLOADS[key]
+    L = w.layers[layer]
+    layer_id = layer + 1000 * copy
+    rng = np.random.default_rng(np.random.SeedSequence([seed, w.config_id, layer_id]))
+    signs, exps, x16, idx = _draw(rng, L.q, L.N, L.K, w.group, batch, w.exp_range,
+                                  w.outlier_fraction, w.outlier_scale)
+    return dict(signs=signs, exps=exps, x=x16, outlier_channels=idx,
+                q=L.q, N=L.N, K=L.K, G=w.group, B=batch,
+                name=f"{key}/{L.name}", seed=seed, copy=copy)
+
+
+def random_case(q: int, N: int, K: int, G: int, B: int, seed: int = 0,
+                exp_range: Tuple[int, int] = (-8, -2), outlier_fraction: float = 0.0,
+                outlier_scale: float = 20.0, x_scale: float = 1.0) -> dict:
+    """A seeded layer of arbitrary shape (parity and edge cases)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 100, q, N, K, G, B]))
+    signs, exps, x16, idx = _draw(rng, q, N, K, G, B, exp_range, outlier_fraction,
+                                  outlier_scale)
+    if x_scale != 1.0:
+        x16 = (x16.astype(np.float64) * x_scale).astype(np.float16)
+    return dict(signs=signs, exps=exps, x=x16, outlier_channels=idx, q=q, N=N, K=K, G=G, B=B,
+                name=f"case(q={q},N={N},K={K},G={G},B={B},seed={seed})", seed=seed, copy=0)
+
