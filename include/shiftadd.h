@@ -1,0 +1,166 @@
+/*
+ * shiftadd.h -- C ABI of the MI355X (gfx950) shift-add linear layer.
+ *
+ * The layer is the inference step of ShiftAddLLM (Sec. 4.1, "Post-training
+ * Reparameterization of LLMs"): a weight matrix quantized into q binary
+ * matrices b_i in {-1,+1}^{N x K} with power-of-two scaling factors (BCQ,
+ * Sec. 3; PoT factors, Eq. 2) is applied to an fp16 activation x by
+ *   (1) shifting by the power-of-two factors, and
+ *   (2) querying 256-entry tables of precomputed partial sums -- one table per
+ *       8 consecutive activations, keyed by 8 binary weights -- and adding.
+ *
+ * What is computed, for b < batch, n < N (fp32 result):
+ *
+ *   y[b][n] = sum_{i<q} sum_{g<K/group} 2^exps[i][n][g] *
+ *             sum_{k = g*group}^{(g+1)*group - 1} s_i[n][k] * x[b][k]
+ *
+ * One exponent per (plane i, output row n, group g of `group` consecutive input
+ * columns).  The sign of each scaling factor is folded into its plane (exact,
+ * because entries are +-1), so exponents carry magnitudes only.  The shift is
+ * applied to each group's fp32 partial sum (ldexp), which equals shifting the
+ * activations because the factor is constant over the group.
+ *
+ * Key convention (Sec. 4.1, "every eight grouped binary weights form an 8-bit
+ * key"; the bit order is this library's reading): the key of chunk c of a plane
+ * row is sum_{j<8} [s[8c+j] = +1] << j -- bit j stands for column 8c+j, a set
+ * bit means +1.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers marked (device) are device memory of the current HIP device; the
+ *    caller allocates and owns every buffer.  `stream` is a hipStream_t passed
+ *    as void* (NULL = the null stream).
+ *  - Arguments are validated on the host before any HIP call; a rejected call
+ *    returns a negative sa_status and enqueues nothing.
+ *  - Accepted calls are asynchronous on `stream`; kernel faults surface at the
+ *    caller's next synchronization.  SA_ERR_HIP reports a launch error.
+ *  - Only int, size_t, fixed-width integers and plain pointers cross the ABI.
+ */
+#ifndef SHIFTADD_H
+#define SHIFTADD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define SA_API __attribute__((visibility("default")))
+#else
+#define SA_API
+#endif
+
+typedef enum {
+    SA_OK = 0,
+    SA_ERR_NULL = -1,  /* a required pointer is NULL */
+    SA_ERR_SHAPE = -2, /* N, K or batch out of range, K % 8 != 0, or sizes overflow */
+    SA_ERR_Q = -3,     /* q outside [1, 8] */
+    SA_ERR_GROUP = -4, /* group < 8, group % 8 != 0, or K % group != 0 */
+    SA_ERR_ALIGN = -5, /* a pointer that must be 16-byte aligned is not */
+    SA_ERR_HIP = -6,   /* a HIP runtime call or kernel launch failed */
+    SA_ERR_NOMEM = -7  /* the split-K workspace could not be allocated */
+} sa_status;
+
+/* Largest accepted values. */
+#define SA_MAX_Q 8
+#define SA_MAX_BATCH 256
+
+/* Bytes of the packed planes of a q x N x K layer: q*N*K/8 (1 bit per weight
+ * per plane, no padding).  Returns 0 for invalid sizes. */
+SA_API size_t sa_packed_bytes(int q, int N, int K);
+
+/* Byte offset, inside the packed buffer, of the key of (plane i, row n,
+ * chunk c) -- chunk c covers columns 8c..8c+7.  Host-only, no HIP call; lets a
+ * caller (or a test) map the device layout to the canonical [q][N][K/8] order.
+ * Returns -1 for out-of-range arguments.
+ *
+ * Device layout: rows in tiles of 64, chunks in blocks of 16.  For tile T with
+ * R = min(64, N - 64T) rows and block J with U = min(16, K/8 - 16J) chunks,
+ *   offset = i*N*(K/8) + 64T*(K/8) + 16J*R + r*U + p,   r = n - 64T,
+ * where position p of a full block (U = 16) holds chunk 16J + ((p + r) mod 16)
+ * and position p of a partial block holds chunk 16J + p.  A 64-row tile of one
+ * 16-chunk block is thus one contiguous 1 KiB piece, 16 bytes per row. */
+SA_API int64_t sa_packed_offset(int q, int N, int K, int i, int n, int c);
+
+/* Pack binary planes into the device layout above (the offline step that
+ * produces the stored form of the b_i of Sec. 3).
+ *   signs        (device) int8 [q][N][K], row-major; > 0 means +1, anything
+ *                else -1.  Any alignment.
+ *   packed_bits  (device) sa_packed_bytes(q, N, K) bytes, 16-byte aligned;
+ *                fully overwritten.
+ * Bit-exact: unpacking returns the signs. */
+SA_API int sa_pack_weights(const int8_t *signs, int q, int N, int K,
+                           uint8_t *packed_bits, void *stream);
+
+/* Inverse of sa_pack_weights: signs[i][n][k] in {-1, +1} (device, int8
+ * [q][N][K], any alignment, fully overwritten). */
+SA_API int sa_unpack_weights(const uint8_t *packed_bits, int q, int N, int K,
+                             int8_t *signs, void *stream);
+
+/* The tables of Sec. 4.1 ("pre-compute 256 possible values for every eight
+ * elements"): for b < batch, c < K/8, m < 256,
+ *   lut[b][c][m] = sum_{j<8} (bit j of m ? +1 : -1) * x[b][8c+j]
+ * computed in fp32 from the fp16 activations.  Entry m and entry 255-m are
+ * exact negatives of each other.  This is the same construction the fused
+ * kernel stages in on-chip memory; it is exposed for inspection and tests.
+ *   x    (device) IEEE binary16 bit patterns [batch][K], row-major, 16-byte
+ *        aligned.
+ *   lut  (device) fp32 [batch][K/8][256], 16-byte aligned, fully overwritten. */
+SA_API int sa_build_lut(const uint16_t *x, int K, int batch, float *lut, void *stream);
+
+/* The layer (Sec. 4.1: shift, then query and add), y = x W_q^T in fp32.
+ *   x            (device) binary16 [batch][K], row-major, 16-byte aligned.
+ *   packed_bits  (device) planes packed by sa_pack_weights for the same
+ *                (q, N, K), 16-byte aligned.
+ *   exps         (device) int8 [q][N][K/group], row-major: exponent of the
+ *                power-of-two factor of (plane, row, group).  Any alignment.
+ *                Results follow fp32 ldexp semantics; exponents in [-30, 30]
+ *                never overflow or lose bits to underflow.
+ *   q in [1, 8]; N >= 1; K >= 8, K % 8 == 0; group % 8 == 0, K % group == 0;
+ *   batch in [1, SA_MAX_BATCH].
+ *   y            (device) fp32 [batch][N], 16-byte aligned, fully
+ *                overwritten (no accumulation into prior contents).
+ * The result is deterministic: the same inputs give bit-identical y.
+ *
+ * Workspace: when the input dimension is split across workgroups the partial
+ * sums go to a device buffer that the library allocates on first use, per
+ * (device, stream), and reuses; sa_shutdown() frees it.  The first call on a
+ * stream (or a call needing a larger buffer) therefore allocates and
+ * synchronizes that stream; later calls allocate nothing.  Calls on different
+ * streams may run concurrently; calls on one stream are ordered by it. */
+SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
+                            int q, int N, int K, int group, int batch, float *y, void *stream);
+
+/* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
+typedef struct {
+    int path;            /* 0: generic kernel (any group), 1: split-K table kernel (group % 128 == 0) */
+    int blocks_per_slice;/* 16-chunk (128-column) blocks per workgroup slice of K */
+    int batch_per_pass;  /* batch rows whose tables share on-chip memory in one launch */
+    int passes;          /* launches per call (batch blocks) */
+    int k_slices;        /* workgroups along K for one row range */
+    int row_ranges;      /* workgroups along N */
+    int rows_per_range;  /* output rows per workgroup (multiple of 64) */
+    int workgroups;      /* workgroups per launch */
+    int threads;         /* threads per workgroup */
+    size_t lds_bytes;    /* on-chip memory per workgroup */
+    size_t workspace_bytes; /* split-K workspace needed (0 if none) */
+} sa_plan;
+
+SA_API int sa_plan_gemm(int q, int N, int K, int group, int batch, sa_plan *plan);
+
+/* Human-readable text for a status code (static storage). */
+SA_API const char *sa_status_string(int status);
+
+/* Library version string, e.g. "0.1.0 gfx950". */
+SA_API const char *sa_version(void);
+
+/* Free the split-K workspaces (synchronizes the streams they belong to).  The
+ * library stays usable; the next call allocates again. */
+SA_API void sa_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHIFTADD_H */

@@ -1,0 +1,19 @@
+"""MI355X (gfx950) shift-add linear layer of ShiftAddLLM (Sec. 4.1).
+
+The computation lives in ``libshiftadd.so`` (HIP kernels behind the C ABI of
+``include/shiftadd.h``); :mod:`paper_2406_05981_amd.shiftadd` is its binding.
+Attribute access on this package loads the binding, which raises if the
+library has not been built (``python -m paper_2406_05981_amd.build``).
+"""
+__all__ = [
+    "sa_packed_bytes", "sa_packed_offset", "sa_pack_weights", "sa_unpack_weights",
+    "sa_build_lut", "sa_shiftadd_gemm", "sa_plan_gemm", "sa_status_string", "sa_version",
+    "sa_shutdown", "pack_weights", "shiftadd_gemm", "SaError",
+]
+
+
+def __getattr__(name):
+    if name in __all__:
+        from . import shiftadd
+        return getattr(shiftadd, name)
+    raise AttributeError(name)

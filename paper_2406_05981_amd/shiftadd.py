@@ -1,0 +1,187 @@
+"""Python binding of ``libshiftadd.so`` (argument marshalling only).
+
+Every function has the name of the C entry point it calls (see
+``include/shiftadd.h``).  Tensors must live on the current HIP device; torch is
+used for device memory and streams only -- every step of the layer runs in the
+library's HIP kernels.  A missing library raises at import; a rejected call
+raises :class:`SaError` with the library's status text.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libshiftadd.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -m paper_2406_05981_amd.build` "
+        "(there is no fallback path)")
+
+
+class SaPlan(ctypes.Structure):
+    _fields_ = [
+        ("path", ctypes.c_int),
+        ("blocks_per_slice", ctypes.c_int),
+        ("batch_per_pass", ctypes.c_int),
+        ("passes", ctypes.c_int),
+        ("k_slices", ctypes.c_int),
+        ("row_ranges", ctypes.c_int),
+        ("rows_per_range", ctypes.c_int),
+        ("workgroups", ctypes.c_int),
+        ("threads", ctypes.c_int),
+        ("lds_bytes", ctypes.c_size_t),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+def _bind(lib):
+    P = ctypes.c_void_p
+    I = ctypes.c_int
+    sig = {
+        "sa_packed_bytes": ([I, I, I], ctypes.c_size_t),
+        "sa_packed_offset": ([I, I, I, I, I, I], ctypes.c_int64),
+        "sa_pack_weights": ([P, I, I, I, P, P], I),
+        "sa_unpack_weights": ([P, I, I, I, P, P], I),
+        "sa_build_lut": ([P, I, I, P, P], I),
+        "sa_shiftadd_gemm": ([P, P, P, I, I, I, I, I, P, P], I),
+        "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
+        "sa_status_string": ([I], ctypes.c_char_p),
+        "sa_version": ([], ctypes.c_char_p),
+        "sa_shutdown": ([], None),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+lib = _bind(ctypes.CDLL(LIB_PATH))
+
+SA_OK, SA_ERR_NULL, SA_ERR_SHAPE, SA_ERR_Q, SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_HIP, SA_ERR_NOMEM = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+SA_MAX_Q = 8
+SA_MAX_BATCH = 256
+
+
+class SaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {sa_status_string(status)} (status {status})")
+
+
+def _check(status: int, where: str) -> None:
+    if status != SA_OK:
+        raise SaError(status, where)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, numel: int) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements, got {t.numel()}")
+    return t.data_ptr()
+
+
+def sa_status_string(status: int) -> str:
+    return lib.sa_status_string(int(status)).decode()
+
+
+def sa_version() -> str:
+    return lib.sa_version().decode()
+
+
+def sa_shutdown() -> None:
+    lib.sa_shutdown()
+
+
+def sa_packed_bytes(q: int, N: int, K: int) -> int:
+    return int(lib.sa_packed_bytes(q, N, K))
+
+
+def sa_packed_offset(q: int, N: int, K: int, i: int, n: int, c: int) -> int:
+    return int(lib.sa_packed_offset(q, N, K, i, n, c))
+
+
+def sa_plan_gemm(q: int, N: int, K: int, group: int, batch: int) -> dict:
+    p = SaPlan()
+    _check(lib.sa_plan_gemm(q, N, K, group, batch, ctypes.byref(p)), "sa_plan_gemm")
+    return {name: getattr(p, name) for name, _ in SaPlan._fields_}
+
+
+def sa_pack_weights(signs: torch.Tensor, q: int, N: int, K: int, packed_bits: torch.Tensor,
+                    stream=None) -> None:
+    nbytes = sa_packed_bytes(q, N, K)
+    if nbytes == 0:
+        _check(SA_ERR_SHAPE if 1 <= q <= SA_MAX_Q else SA_ERR_Q, "sa_pack_weights")
+    _check(lib.sa_pack_weights(_dev(signs, "signs", torch.int8, q * N * K), q, N, K,
+                               _dev(packed_bits, "packed_bits", torch.uint8, nbytes),
+                               _stream(stream)), "sa_pack_weights")
+
+
+def sa_unpack_weights(packed_bits: torch.Tensor, q: int, N: int, K: int, signs: torch.Tensor,
+                      stream=None) -> None:
+    nbytes = sa_packed_bytes(q, N, K)
+    if nbytes == 0:
+        _check(SA_ERR_SHAPE if 1 <= q <= SA_MAX_Q else SA_ERR_Q, "sa_unpack_weights")
+    _check(lib.sa_unpack_weights(_dev(packed_bits, "packed_bits", torch.uint8, nbytes), q, N, K,
+                                 _dev(signs, "signs", torch.int8, q * N * K), _stream(stream)),
+           "sa_unpack_weights")
+
+
+def sa_build_lut(x: torch.Tensor, K: int, batch: int, lut: torch.Tensor, stream=None) -> None:
+    _check(lib.sa_build_lut(_dev(x, "x", torch.float16, batch * K), K, batch,
+                            _dev(lut, "lut", torch.float32, batch * (K // 8) * 256),
+                            _stream(stream)), "sa_build_lut")
+
+
+def sa_shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Tensor, q: int,
+                     N: int, K: int, group: int, batch: int, y: torch.Tensor,
+                     stream=None) -> None:
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_shiftadd_gemm")
+    _check(lib.sa_shiftadd_gemm(
+        _dev(x, "x", torch.float16, batch * K),
+        _dev(packed_bits, "packed_bits", torch.uint8, sa_packed_bytes(q, N, K)),
+        _dev(exps, "exps", torch.int8, q * N * (K // group)),
+        q, N, K, group, batch,
+        _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm")
+
+
+# ------------------------------------------------------------------ conveniences
+
+def pack_weights(signs: torch.Tensor, stream=None) -> torch.Tensor:
+    """Packed planes of ``int8 [q][N][K]`` signs (a new uint8 device tensor)."""
+    q, N, K = signs.shape
+    packed = torch.empty(sa_packed_bytes(q, N, K), dtype=torch.uint8, device=signs.device)
+    sa_pack_weights(signs, q, N, K, packed, stream)
+    return packed
+
+
+def shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Tensor, q: int, N: int,
+                  K: int, group: int, out: Optional[torch.Tensor] = None,
+                  stream=None) -> torch.Tensor:
+    """``y = x W_q^T`` as a new (or the given) fp32 ``[batch][N]`` tensor."""
+    batch = x.shape[0] if x.dim() == 2 else 1
+    y = out if out is not None else torch.empty((batch, N), dtype=torch.float32, device=x.device)
+    sa_shiftadd_gemm(x, packed_bits, exps, q, N, K, group, batch, y, stream)
+    return y

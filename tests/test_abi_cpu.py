@@ -1,0 +1,125 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, and
+rejects invalid arguments on the host before any HIP call.  No compute call is
+made here (there is no GPU in this environment)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "shiftadd.h")
+
+sa = pytest.importorskip("paper_2406_05981_amd.shiftadd",
+                         reason="libshiftadd.so not built (python -m paper_2406_05981_amd.build)")
+from tests import _layout  # noqa: E402
+
+A = 1 << 20  # a non-null, 16-byte aligned fake address; never dereferenced here
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SA_API\s+[\w\s\*]+?\b(sa_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_symbols()
+    assert {"sa_pack_weights", "sa_unpack_weights", "sa_build_lut", "sa_shiftadd_gemm",
+            "sa_packed_bytes", "sa_packed_offset", "sa_plan_gemm", "sa_status_string",
+            "sa_version", "sa_shutdown"} <= set(names)
+    raw = ctypes.CDLL(sa.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in sa.sa_version()
+    for st in range(0, -8, -1):
+        assert sa.sa_status_string(st) not in ("", "unknown status")
+    assert sa.sa_status_string(-99) == "unknown status"
+
+
+def test_packed_bytes():
+    assert sa.sa_packed_bytes(3, 4096, 4096) == 3 * 4096 * 512
+    assert sa.sa_packed_bytes(0, 8, 8) == 0
+    assert sa.sa_packed_bytes(9, 8, 8) == 0
+    assert sa.sa_packed_bytes(1, 8, 12) == 0
+
+
+@pytest.mark.parametrize("q,N,K", [(1, 1, 8), (2, 65, 136), (3, 64, 128), (2, 130, 264),
+                                   (1, 200, 1040), (3, 5, 256)])
+def test_layout_is_a_bijection_and_matches_restatement(q, N, K):
+    off = _layout.offsets(q, N, K)
+    assert np.array_equal(np.sort(off.reshape(-1)), np.arange(q * N * (K // 8)))
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        i, n, c = int(rng.integers(q)), int(rng.integers(N)), int(rng.integers(K // 8))
+        assert sa.sa_packed_offset(q, N, K, i, n, c) == off[i, n, c]
+    assert sa.sa_packed_offset(q, N, K, q, 0, 0) == -1
+    assert sa.sa_packed_offset(q, N, K, 0, N, 0) == -1
+    assert sa.sa_packed_offset(q, N, K, 0, 0, K // 8) == -1
+
+
+def test_layout_tiles_are_contiguous_16_byte_rows():
+    """A 64-row tile of a full 16-chunk block is 1 KiB, 16 bytes per row, and
+    position p of row r holds chunk (p + r) mod 16."""
+    q, N, K = 1, 128, 256
+    off = _layout.offsets(q, N, K)
+    for r in (0, 1, 17, 63):
+        row = off[0, r, :16]
+        assert sorted(row.tolist()) == list(range(16 * r, 16 * r + 16))
+        for c in range(16):
+            assert row[c] - 16 * r == (c - r) % 16
+
+
+def _gemm(x=A, p=A, e=A, q=3, N=64, K=256, G=128, B=1, y=A):
+    return sa.lib.sa_shiftadd_gemm(x, p, e, q, N, K, G, B, y, None)
+
+
+def test_gemm_validation_codes():
+    assert _gemm(x=None) == sa.SA_ERR_NULL
+    assert _gemm(p=None) == sa.SA_ERR_NULL
+    assert _gemm(e=None) == sa.SA_ERR_NULL
+    assert _gemm(y=None) == sa.SA_ERR_NULL
+    assert _gemm(q=0) == sa.SA_ERR_Q
+    assert _gemm(q=9) == sa.SA_ERR_Q
+    assert _gemm(N=0) == sa.SA_ERR_SHAPE
+    assert _gemm(K=12) == sa.SA_ERR_SHAPE
+    assert _gemm(K=0) == sa.SA_ERR_SHAPE
+    assert _gemm(B=0) == sa.SA_ERR_SHAPE
+    assert _gemm(B=sa.SA_MAX_BATCH + 1) == sa.SA_ERR_SHAPE
+    assert _gemm(G=0) == sa.SA_ERR_GROUP
+    assert _gemm(G=12) == sa.SA_ERR_GROUP
+    assert _gemm(G=96) == sa.SA_ERR_GROUP  # 256 % 96 != 0
+    assert _gemm(x=A + 8) == sa.SA_ERR_ALIGN
+    assert _gemm(p=A + 4) == sa.SA_ERR_ALIGN
+    assert _gemm(y=A + 2) == sa.SA_ERR_ALIGN
+    assert _gemm(e=A + 1, x=None) == sa.SA_ERR_NULL  # exps may be unaligned; NULL x still caught
+
+
+def test_pack_lut_validation_codes():
+    L = sa.lib
+    assert L.sa_pack_weights(None, 1, 8, 8, A, None) == sa.SA_ERR_NULL
+    assert L.sa_pack_weights(A, 1, 8, 8, None, None) == sa.SA_ERR_NULL
+    assert L.sa_pack_weights(A, 0, 8, 8, A, None) == sa.SA_ERR_Q
+    assert L.sa_pack_weights(A, 1, 8, 9, A, None) == sa.SA_ERR_SHAPE
+    assert L.sa_pack_weights(A, 1, 8, 8, A + 1, None) == sa.SA_ERR_ALIGN
+    assert L.sa_unpack_weights(None, 1, 8, 8, A, None) == sa.SA_ERR_NULL
+    assert L.sa_unpack_weights(A, 1, -1, 8, A, None) == sa.SA_ERR_SHAPE
+    assert L.sa_build_lut(None, 8, 1, A, None) == sa.SA_ERR_NULL
+    assert L.sa_build_lut(A, 10, 1, A, None) == sa.SA_ERR_SHAPE
+    assert L.sa_build_lut(A, 8, 0, A, None) == sa.SA_ERR_SHAPE
+    assert L.sa_build_lut(A + 2, 8, 1, A, None) == sa.SA_ERR_ALIGN
+
+
+def test_plans():
+    p = sa.sa_plan_gemm(3, 4096, 4096, 128, 1)
+    assert p["path"] == 1 and p["workgroups"] == p["k_slices"] * p["row_ranges"]
+    assert p["rows_per_range"] % 64 == 0 and p["workgroups"] >= 256
+    assert sa.sa_plan_gemm(3, 100, 256, 8, 2)["path"] == 0
+    assert sa.sa_plan_gemm(3, 100, 768, 768, 2)["path"] == 1
+    p16 = sa.sa_plan_gemm(2, 4096, 11008, 128, 16)
+    assert p16["passes"] == 4 and p16["batch_per_pass"] == 4
+    with pytest.raises(sa.SaError):
+        sa.sa_plan_gemm(3, 100, 256, 24, 1)

@@ -75,3 +75,12 @@ def test_golden_small_cases(oracle_mod):
         y, a = oracle_mod.shiftadd_gemm(c["x"], c["signs"], c["exps"], s["G"])
         assert [[v.hex() for v in row] for row in y] == case["y"]
         assert [[v.hex() for v in row] for row in a] == case["absterm"]
+
+
+def test_layer_inputs_batches_matches_single_draws():
+    d = workloads.layer_inputs_batches("llama2_7b_attn", 0, (1, 3))
+    for B in (1, 3):
+        e = workloads.layer_inputs("llama2_7b_attn", 0, B)
+        assert np.array_equal(d["x"][B], e["x"])
+        assert np.array_equal(d["exps"], e["exps"])
+    assert workloads.sha256(d["signs"]) == workloads.sha256(e["signs"])

@@ -8,7 +8,8 @@ What is drawn, per layer of shape N x K with q binary planes and group size G
 (ShiftAddLLM, Sec. 3 "Binary-coding Quantization" and Sec. 4.1):
 
 * ``signs``  int8 ``[q][N][K]`` in {-1, +1}: the binary matrices b_i, each entry
-  an independent fair coin (the Bernoulli(0.5) planes of the synthetic layers).
+  an independent fair coin (the Bernoulli(0.5) planes of the synthetic layers),
+  taken from the bits of uniformly random bytes.
 * ``exps``   int8 ``[q][N][K/G]``: the power-of-two exponents P of the scaling
   factors 2^P (Eq. 2), uniform over an inclusive integer range.  The sign of a
   scaling factor is assumed folded into the plane, so only magnitudes remain.
@@ -37,6 +38,7 @@ __all__ = [
     "WORKLOADS",
     "workload",
     "layer_inputs",
+    "layer_inputs_batches",
     "random_case",
     "mixed_bits",
     "sha256",
@@ -129,21 +131,34 @@ def sha256(a: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
 
 
-def _draw(rng: np.random.Generator, q: int, N: int, K: int, G: int, B: int,
-          exp_range: Tuple[int, int], outlier_fraction: float, outlier_scale: float):
-    # signs: fair coins mapped to {-1, +1}
-    signs = rng.integers(0, 2, size=(q, N, K), dtype=np.int8)
+def _draw_weights(rng: np.random.Generator, q: int, N: int, K: int, G: int,
+                  exp_range: Tuple[int, int]):
+    # signs: fair coins mapped to {-1, +1}; the coins are the bits of uniformly
+    # random bytes (8 coins per byte drawn)
+    coins = np.unpackbits(rng.integers(0, 256, size=(q, N, K // 8), dtype=np.uint8),
+                          axis=-1, bitorder="little")
+    signs = coins.view(np.int8)
     signs *= 2
     signs -= 1
     exps = rng.integers(exp_range[0], exp_range[1] + 1, size=(q, N, K // G), dtype=np.int8)
+    return signs, exps
+
+
+def _draw_x(rng: np.random.Generator, K: int, B: int, outlier_fraction: float,
+            outlier_scale: float):
     x = rng.standard_normal((B, K))
     n_out = int(round(outlier_fraction * K))
     idx = np.zeros(0, dtype=np.int64)
     if n_out > 0:
         idx = rng.choice(K, size=n_out, replace=False)
         x[:, idx] *= outlier_scale
-    x16 = x.astype(np.float16)
-    return signs, exps, x16, np.sort(idx)
+    return x.astype(np.float16), np.sort(idx)
+
+
+def _draw(rng, q, N, K, G, B, exp_range, outlier_fraction, outlier_scale):
+    signs, exps = _draw_weights(rng, q, N, K, G, exp_range)
+    x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
+    return signs, exps, x16, idx
 
 
 def layer_inputs(key: str, layer: int, batch: int, seed: int = 0, copy: int = 0) -> dict:
@@ -162,6 +177,26 @@ def layer_inputs(key: str, layer: int, batch: int, seed: int = 0, copy: int = 0)
                                   w.outlier_fraction, w.outlier_scale)
     return dict(signs=signs, exps=exps, x=x16, outlier_channels=idx,
                 q=L.q, N=L.N, K=L.K, G=w.group, B=batch,
+                name=f"{key}/{L.name}", seed=seed, copy=copy)
+
+
+def layer_inputs_batches(key: str, layer: int, batches: Sequence[int], seed: int = 0,
+                         copy: int = 0) -> dict:
+    """One draw of a layer's weights with the activations of several batch sizes.
+
+    ``x[B]`` equals ``layer_inputs(key, layer, B, seed, copy)["x"]``: the
+    activations are drawn from the generator state right after the weights.
+    """
+    w = WORKLOADS[key]
+    L = w.layers[layer]
+    rng = np.random.default_rng(np.random.SeedSequence([seed, w.config_id, layer + 1000 * copy]))
+    signs, exps = _draw_weights(rng, L.q, L.N, L.K, w.group, w.exp_range)
+    state = rng.bit_generator.state
+    xs = {}
+    for B in batches:
+        rng.bit_generator.state = state
+        xs[B] = _draw_x(rng, L.K, B, w.outlier_fraction, w.outlier_scale)[0]
+    return dict(signs=signs, exps=exps, x=xs, q=L.q, N=L.N, K=L.K, G=w.group,
                 name=f"{key}/{L.name}", seed=seed, copy=copy)
 
 
