@@ -476,45 +476,62 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     p->rows_per_range = tiles_per_range * kTileRows;
     p->workgroups = row_ranges * k_slices;
     p->lds_bytes = sizeof(float) * 256 * kKeyStride;
-    if (k_slices > 1) {
-        const size_t tickets = ((size_t)tiles * sizeof(unsigned) + 255) & ~(size_t)255;
-        p->workspace_bytes = tickets + sizeof(float) * (size_t)k_slices * first.bb * N;
-    }
+    if (k_slices > 1)
+        p->workspace_bytes =
+            sizeof(unsigned) * (size_t)tiles + sizeof(float) * (size_t)k_slices * first.bb * N;
 }
 
-// Split-K workspace per (device, stream): [tickets | partials].  Tickets are
-// zeroed once at allocation; kernels leave them at zero.
+// Split-K workspace per (device, stream): a ticket array (one counter per
+// 64-row tile) and a partial-sum array, in separate buffers.  Tickets are
+// zeroed when their buffer is allocated and every call leaves them at zero;
+// nothing else is ever written to the ticket buffer.
 struct Workspace {
-    void* ptr = nullptr;
-    size_t bytes = 0;
+    unsigned* tickets = nullptr;
+    size_t ticket_count = 0;
+    float* partials = nullptr;
+    size_t partial_bytes = 0;
 };
 std::mutex g_mu;
 std::map<std::pair<int, void*>, Workspace> g_ws;
 
-int get_workspace(void* stream, size_t bytes, void** out) {
+int get_workspace(void* stream, size_t tickets, size_t partial_bytes, unsigned** t_out,
+                  float** p_out) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
     std::lock_guard<std::mutex> lock(g_mu);
     Workspace& w = g_ws[{dev, stream}];
-    if (w.bytes < bytes) {
-        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        if (w.ptr) {
-            if (hipStreamSynchronize(s) != hipSuccess) return SA_ERR_HIP;
-            (void)hipFree(w.ptr);
-            w.ptr = nullptr;
-            w.bytes = 0;
-        }
-        size_t want = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool grow_t = w.ticket_count < tickets, grow_p = w.partial_bytes < partial_bytes;
+    if ((grow_t && w.tickets) || (grow_p && w.partials)) {
+        if (hipStreamSynchronize(s) != hipSuccess) return SA_ERR_HIP;
+    }
+    if (grow_t) {
+        if (w.tickets) (void)hipFree(w.tickets);
+        w.tickets = nullptr;
+        w.ticket_count = 0;
+        size_t want = tickets < 4096 ? 4096 : tickets;
         void* p = nullptr;
-        if (hipMalloc(&p, want) != hipSuccess) return SA_ERR_NOMEM;
-        if (hipMemsetAsync(p, 0, want, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
+        if (hipMalloc(&p, want * sizeof(unsigned)) != hipSuccess) return SA_ERR_NOMEM;
+        if (hipMemsetAsync(p, 0, want * sizeof(unsigned), s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess) {
             (void)hipFree(p);
             return SA_ERR_HIP;
         }
-        w.ptr = p;
-        w.bytes = want;
+        w.tickets = static_cast<unsigned*>(p);
+        w.ticket_count = want;
     }
-    *out = w.ptr;
+    if (grow_p) {
+        if (w.partials) (void)hipFree(w.partials);
+        w.partials = nullptr;
+        w.partial_bytes = 0;
+        size_t want = partial_bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : partial_bytes;
+        void* p = nullptr;
+        if (hipMalloc(&p, want) != hipSuccess) return SA_ERR_NOMEM;
+        w.partials = static_cast<float*>(p);
+        w.partial_bytes = want;
+    }
+    *t_out = w.tickets;
+    *p_out = w.partials;
     return SA_OK;
 }
 
@@ -603,13 +620,14 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
                            x, packed_bits, exps, q, N, K, group, y);
         return launch_status();
     }
-    void* ws = nullptr;
+    const int tiles = (N + kTileRows - 1) / kTileRows;
+    unsigned* tickets = nullptr;
+    float* partials = nullptr;
     if (plan.workspace_bytes > 0) {
-        const int wst = get_workspace(stream, plan.workspace_bytes, &ws);
+        const size_t pbytes = plan.workspace_bytes - sizeof(unsigned) * (size_t)tiles;
+        const int wst = get_workspace(stream, (size_t)tiles, pbytes, &tickets, &partials);
         if (wst != SA_OK) return wst;
     }
-    const int tiles = (N + kTileRows - 1) / kTileRows;
-    const size_t ticket_bytes = ((size_t)tiles * sizeof(unsigned) + 255) & ~(size_t)255;
     SplitKArgs a{};
     a.x_stride = K;
     a.packed = packed_bits;
@@ -619,8 +637,8 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.K = K;
     a.G = group;
     a.y_stride = N;
-    a.tickets = reinterpret_cast<unsigned*>(ws);
-    a.partials = ws ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + ticket_bytes) : nullptr;
+    a.tickets = tickets;
+    a.partials = partials;
     a.row_ranges = plan.row_ranges;
     a.tiles_per_range = plan.rows_per_range / kTileRows;
     for (int b0 = 0; b0 < batch;) {
@@ -662,16 +680,15 @@ SA_API const char* sa_version(void) { return SA_VERSION_STRING; }
 
 SA_API void sa_shutdown(void) {
     std::lock_guard<std::mutex> lock(g_mu);
+    int cur = 0;
+    (void)hipGetDevice(&cur);
     for (auto& kv : g_ws) {
-        if (kv.second.ptr) {
-            int cur = 0;
-            (void)hipGetDevice(&cur);
-            (void)hipSetDevice(kv.first.first);
-            (void)hipStreamSynchronize(reinterpret_cast<hipStream_t>(kv.first.second));
-            (void)hipFree(kv.second.ptr);
-            (void)hipSetDevice(cur);
-        }
+        (void)hipSetDevice(kv.first.first);
+        (void)hipStreamSynchronize(reinterpret_cast<hipStream_t>(kv.first.second));
+        if (kv.second.tickets) (void)hipFree(kv.second.tickets);
+        if (kv.second.partials) (void)hipFree(kv.second.partials);
     }
+    (void)hipSetDevice(cur);
     g_ws.clear();
 }
 

@@ -286,3 +286,15 @@ def test_binding_raises_on_bad_arguments():
         sa.sa_shiftadd_gemm(x, packed, e, 3, 64, 256, 128, 1, ybig)  # wrong numel
     with pytest.raises(sa.SaError):
         sa.sa_shiftadd_gemm(x, packed, e, 3, 64, 256, 96, 1, ybig[:64])
+
+
+def test_tickets_survive_smaller_earlier_calls():
+    """Regression: a call with few 64-row tiles and large partial sums, followed
+    by a call with more tiles on the same stream.  The second call's tile
+    tickets must not alias the first call's partial sums."""
+    say("ticket aliasing regression")
+    first = workloads.random_case(2, 1000, 4096, 128, 16, seed=16)
+    second = workloads.random_case(3, 4097, 512, 128, 1, seed=17)
+    for c in (first, second, first, second):
+        y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], 128)
+        check(gemm(c), y_ref, a_ref, c["name"])
