@@ -58,8 +58,7 @@ typedef enum {
     SA_ERR_Q = -3,     /* q outside [1, 8] */
     SA_ERR_GROUP = -4, /* group < 8, group % 8 != 0, or K % group != 0 */
     SA_ERR_ALIGN = -5, /* a pointer that must be 16-byte aligned is not */
-    SA_ERR_HIP = -6,   /* a HIP runtime call or kernel launch failed */
-    SA_ERR_NOMEM = -7  /* the split-K workspace could not be allocated */
+    SA_ERR_HIP = -6    /* a HIP runtime call or kernel launch failed */
 } sa_status;
 
 /* Largest accepted values. */
@@ -121,30 +120,21 @@ SA_API int sa_build_lut(const uint16_t *x, int K, int batch, float *lut, void *s
  *   batch in [1, SA_MAX_BATCH].
  *   y            (device) fp32 [batch][N], 16-byte aligned, fully
  *                overwritten (no accumulation into prior contents).
- * The result is deterministic: the same inputs give bit-identical y.
- *
- * Workspace: when the input dimension is split across workgroups the partial
- * sums go to a device buffer that the library allocates on first use, per
- * (device, stream), and reuses; sa_shutdown() frees it.  The first call on a
- * stream (or a call needing a larger buffer) therefore allocates and
- * synchronizes that stream; later calls allocate nothing.  Calls on different
- * streams may run concurrently; calls on one stream are ordered by it. */
+ * The result is deterministic: the same inputs give bit-identical y.  The call
+ * allocates nothing, keeps no state between calls and uses no memory beyond
+ * its arguments, so calls on different streams may run concurrently and the
+ * call may be captured in a HIP graph. */
 SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
                             int q, int N, int K, int group, int batch, float *y, void *stream);
 
 /* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
 typedef struct {
-    int path;            /* 0: generic kernel (any group), 1: split-K table kernel (group % 128 == 0) */
-    int blocks_per_slice;/* 16-chunk (128-column) blocks per workgroup slice of K */
-    int batch_per_pass;  /* batch rows whose tables share on-chip memory in one launch */
-    int passes;          /* launches per call (batch blocks) */
-    int k_slices;        /* workgroups along K for one row range */
-    int row_ranges;      /* workgroups along N */
-    int rows_per_range;  /* output rows per workgroup (multiple of 64) */
-    int workgroups;      /* workgroups per launch */
-    int threads;         /* threads per workgroup */
-    size_t lds_bytes;    /* on-chip memory per workgroup */
-    size_t workspace_bytes; /* split-K workspace needed (0 if none) */
+    int path;         /* 0: generic kernel (any group), 1: row kernel (group % 128 == 0) */
+    int rows_per_wg;  /* output rows per workgroup */
+    int workgroups;   /* workgroups of the launch */
+    int threads;      /* threads per workgroup */
+    int pieces;       /* input-dimension pieces whose tables a workgroup builds in turn */
+    size_t lds_bytes; /* on-chip memory per workgroup */
 } sa_plan;
 
 SA_API int sa_plan_gemm(int q, int N, int K, int group, int batch, sa_plan *plan);
@@ -154,10 +144,6 @@ SA_API const char *sa_status_string(int status);
 
 /* Library version string, e.g. "0.1.0 gfx950". */
 SA_API const char *sa_version(void);
-
-/* Free the split-K workspaces (synchronizes the streams they belong to).  The
- * library stays usable; the next call allocates again. */
-SA_API void sa_shutdown(void);
 
 #ifdef __cplusplus
 }

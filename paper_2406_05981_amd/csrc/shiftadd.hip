@@ -10,9 +10,6 @@
 
 #include <stdint.h>
 
-#include <map>
-#include <mutex>
-#include <utility>
 
 #include "shiftadd.h"
 
@@ -188,216 +185,306 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
     if (active) y[(int64_t)b * N + n] = total;
 }
 
-// ---------------------------------------------------------------- split-K table kernel
+// ---------------------------------------------------------------- row kernel
 //
-// group % 128 == 0.  Workgroup (range, slice): output rows of `range` (tiles of
-// 64 rows, one row per lane, one tile per wave at a time) against the
-// 128*GB input columns of `slice` (GB blocks of 16 chunks).
+// group % 128 == 0.  Each workgroup owns 16*rg_per_wg output rows over the
+// whole input dimension, so no partial sums ever leave a workgroup.
 //
-// LDS tables: key m of table slot s (slot = 16*block + chunk within block) for
-// batch row bb is the float at byte m*256 + 4*(s*BB + bb).  A lane queries with
-// one v_perm_b32 that places its key byte in bits 8..15 and its slot offset in
-// bits 0..7 of the address.  Lanes 16l..16l+15 query block (j + l) mod nb at
-// step j, and, through the rotated packed layout, 16 different chunks of it at
-// each position, so the 32 lanes of a half-wave read 32 different slots: 32
-// different banks.
+// Tables.  The 256-entry table of chunk c (Sec. 4.1) is stored factored into
+// its two 16-entry halves: lo_c[v] = sum_{j<4} (bit j of v ? +x : -x)[8c+j] and
+// hi_c[v] likewise over columns 8c+4..8c+7, so entry m = lo_c[m & 15] +
+// hi_c[m >> 4].  A query of key m reads both halves and adds them.  32 stored
+// values per chunk instead of 256 let one workgroup hold the tables of 4096
+// columns in 64 KB of LDS and build them in a fraction of the time the
+// queries take.
 //
-// Each lane adds 16 queried entries (one block of one plane), shifts the sum by
-// the exponent of its (plane, row, group) with ldexp and accumulates in fp32.
-// Slices of one row tile meet through a workspace: every wave writes its tile's
-// partial sums, and the last of the k_slices waves to finish a tile (atomic
-// ticket) adds them in slice order and writes y.  The order is fixed, so the
-// result is deterministic.
+// LDS layout of a 4096-column piece: 16 regions of 4 KB (two 16-chunk blocks
+// each); value v of half-table `slot` of region rho is the float at byte
+// rho*4096 + v*256 + slot*4.  A query address is one v_perm_b32: byte 1 =
+// (rho << 4) | v (key nibble, region pre-or'ed into the key word), byte 0 =
+// 4*slot.  Slots: chunk u of the region's even block -> (2u, 2u+1) for (lo, hi),
+// odd block -> 32 + (2u+1, 2u) (swapped), odd regions -> slot ^ 32.
+//
+// Work split.  Row r of a 16-row group is handled by lanes r, r+16, r+32,
+// r+48 of all four waves: part = 4*wave + (lane >> 4) owns the blocks
+// J = part + 16k of each piece.  Keys are stored rotated by row (position t of
+// a row's 16 bytes holds chunk (t + row) mod 16), so at each query the 32
+// lanes of a half-wave touch 32 different slots mod 32 (and the 64 lanes 64
+// different slots mod 64): no LDS bank conflicts by construction.
+//
+// Each lane adds the 32 half-entries of one block, shifts the sum by the
+// block's exponent (ldexp) and accumulates in fp32; the 16 lanes of a row are
+// then combined in a fixed order (two xor-shuffles, then the four waves via
+// LDS).  The result is deterministic.
 
-struct SplitKArgs {
-    const uint16_t* x;     // activations of this pass, rows b0..b0+nbr-1
-    int x_stride;          // elements between batch rows (K)
-    int nbr;               // batch rows in this pass (<= BB)
+constexpr int kGroupRows = 16;       // rows per row group
+constexpr int kPieceBlocks = 32;     // 128-column blocks per table piece (4096 columns)
+constexpr int kPieceChunks = kPieceBlocks * kBlockChunks;
+constexpr int kRegionFloats = 1024;  // 4 KB: 16 values x 64 slots
+constexpr int kMaxRG = 8;            // row groups per workgroup
+
+struct RowsArgs {
+    const uint16_t* x;  // activations [B][K]
     const uint8_t* packed;
     const int8_t* exps;
-    int q, N, K, G;
-    float* y;              // output rows of this pass
-    int y_stride;          // elements between batch rows (N)
-    float* partials;       // [k_slices][BB][N]
-    unsigned* tickets;     // [ceil(N/64)], zero between calls
-    int k_slices, row_ranges, tiles_per_range;
+    int q, N, K, G, B;
+    float* y;           // [B][N]
+    int rg_per_wg;      // row groups per workgroup (<= kMaxRG)
 };
 
-template <int BB>
-__device__ inline void query_add(const char* lut_bytes, uint32_t addr, float acc[BB]) {
-    if constexpr (BB == 1) {
-        acc[0] += *reinterpret_cast<const float*>(lut_bytes + addr);
-    } else if constexpr (BB == 2) {
-        const float2 v = *reinterpret_cast<const float2*>(lut_bytes + addr);
-        acc[0] += v.x;
-        acc[1] += v.y;
-    } else {
-        const float4 v = *reinterpret_cast<const float4*>(lut_bytes + addr);
-        acc[0] += v.x;
-        acc[1] += v.y;
-        acc[2] += v.z;
-        acc[3] += v.w;
+// Keys and exponents of one (row group, piece) job for this lane: Q planes x 2 blocks.
+template <int Q>
+struct JobRegs {
+    uint4 w[Q][2];
+    int e[Q][2];  // exponent (sign-extending byte load)
+};
+
+// Exponents are requested before keys (and, for the first job, before the
+// activations): whatever the compiler hoists onto the exponents then waits for
+// them alone, never for the keys behind them.
+template <int Q>
+__device__ inline void load_job_exps(const RowsArgs& a, int rg, int pc, int part, int r, int C16,
+                                     int NG, int bpg, JobRegs<Q>& j) {
+    const int n = imin(kGroupRows * rg + r, a.N - 1);
+    const int8_t* erow_base = a.exps + (int64_t)n * NG;
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+        const int8_t* erow = erow_base + (int64_t)i * a.N * NG;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int J = imin(kPieceBlocks * pc + part + 16 * k, C16 - 1);
+            j.e[i][k] = erow[J / bpg];
+        }
     }
 }
 
-template <int GB, int BB>
-__global__ __launch_bounds__(kThreads) void k_gemm_splitk(SplitKArgs a) {
-    static_assert(kBlockChunks * GB * BB <= kKeyStride, "slot offsets must fit in one byte");
-    __shared__ float lut[256 * kKeyStride];
+template <int Q>
+__device__ inline void load_job_keys(const RowsArgs& a, int rg, int pc, int part, int r, int C,
+                                     int C16, JobRegs<Q>& j) {
+    const int n = imin(kGroupRows * rg + r, a.N - 1);
+    const int T = n >> 6;
+    const int R = imin(kTileRows, a.N - kTileRows * T);
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+        const uint8_t* base =
+            a.packed + ((int64_t)i * a.N + (int64_t)kTileRows * T) * C + 16 * (n & 63);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int J = imin(kPieceBlocks * pc + part + 16 * k, C16 - 1);
+            j.w[i][k] = *reinterpret_cast<const uint4*>(base + (int64_t)kBlockChunks * J * R);
+        }
+    }
+}
+
+// Empty asm that "may modify" one plane's job registers: their consumers
+// cannot be hoisted above this point, so the wait for that plane's loads lands
+// here -- after the tables are built and after the previous plane's queries.
+template <int Q>
+__device__ inline void pin_plane(JobRegs<Q>& j, int i) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+        asm volatile("" : "+v"(j.w[i][k].x), "+v"(j.w[i][k].y), "+v"(j.w[i][k].z),
+                     "+v"(j.w[i][k].w), "+v"(j.e[i][k]));
+}
+
+// Queries and adds of one job; returns sum over planes and owned blocks of
+// ldexp(block sum, exponent).  Planes are consumed in load order, so a plane's
+// queries run while later planes are still arriving.
+template <int Q>
+__device__ inline float job_sum(JobRegs<Q>& j, const bool valid[2], const uint32_t rgn[2],
+                                const uint32_t offs[2][4], const char* lut_bytes) {
+    float tot = 0.0f;
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+        pin_plane<Q>(j, i);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const uint32_t words[4] = {j.w[i][k].x, j.w[i][k].y, j.w[i][k].z, j.w[i][k].w};
+            float acc = 0.0f;
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+                // key nibbles of 4 bytes, each or'ed with this block's region
+                const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn[k];
+                const uint32_t hi = ((words[wd] >> 4) & 0x0f0f0f0fu) | rgn[k];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    // byte 0: slot offset (offs byte t); byte 1: region|nibble (byte t)
+                    const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                    acc += *reinterpret_cast<const float*>(
+                        lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
+                    acc += *reinterpret_cast<const float*>(
+                        lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
+                }
+            }
+            const float v = ldexpf(acc, j.e[i][k]);
+            tot += valid[k] ? v : 0.0f;
+        }
+    }
+    return tot;
+}
+
+template <int Q>
+__global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kThreads / 64][kGroupRows * kMaxRG];
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
-
-    // Workgroup -> (range, slice).  Workgroups are dispatched round-robin over
-    // the 8 XCDs; when row_ranges % 8 == 0 every slice of a range lands on the
-    // same XCD, so they share its L2 for exponents and partial sums.
-    int range, slice;
-    {
-        const int w = blockIdx.x;
-        if ((a.row_ranges & 7) == 0) {
-            const int xcd = w & 7, u = w >> 3;
-            slice = u % a.k_slices;
-            range = ((u / a.k_slices) << 3) | xcd;
-        } else {
-            range = w / a.k_slices;
-            slice = w % a.k_slices;
-        }
-    }
-    const int J0 = slice * GB;
-    const int nb = imin(GB, C16 - J0);
-    const int ncol = kBlockChunks * nb * BB;
-
-    // ---- tables for this slice: item (column, quarter of the high nibbles)
-    for (int t = threadIdx.x; t < ncol * 4; t += kThreads) {
-        const int col = t % ncol, hq = t / ncol;
-        const int bb = col % BB, slot = col / BB;
-        const int c = kBlockChunks * (J0 + (slot >> 4)) + (slot & 15);
-        float f[8];
-        if (bb < a.nbr) {
-            load_chunk(a.x + (int64_t)bb * a.x_stride + 8 * c, f);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) f[j] = 0.0f;
-        }
-        float lo[16];
-        nibble_sums(f[0], f[1], f[2], f[3], lo);
-#pragma unroll
-        for (int hh = 0; hh < 4; ++hh) {
-            const int h = 4 * hq + hh;
-            const float hi = nibble_sum(f[4], f[5], f[6], f[7], h);
-#pragma unroll
-            for (int m = 0; m < 16; ++m) lut[(16 * h + m) * kKeyStride + col] = lo[m] + hi;
-        }
-    }
-    __syncthreads();
-
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    // Block of register slot j for this lane, and the slot offsets of its 16
-    // positions (4 per register, one per byte).
-    int blk[GB];
-    uint32_t offs[GB][4];
+    const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
+    const int rg0 = blockIdx.x * a.rg_per_wg;
+    const int n_groups = (a.N + kGroupRows - 1) / kGroupRows;
+    const int nrg = imin(a.rg_per_wg, n_groups - rg0);
+    const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
+
+    // Slot offsets of this lane's 16 key positions, low and high nibble (4
+    // positions per register, one per byte), and the region bits of its two
+    // blocks, replicated in every byte's high nibble.
+    uint32_t offs[2][4];
 #pragma unroll
-    for (int j = 0; j < GB; ++j) {
-        const int g = nb > 0 ? (j + (lane >> 4)) % nb : 0;
-        blk[j] = J0 + g;
+    for (int nb = 0; nb < 2; ++nb) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int wd = 0; wd < 4; ++wd) {
             uint32_t v = 0;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const int p = 4 * k + t;
-                const uint32_t s = (uint32_t)(kBlockChunks * g + ((p + lane) & 15));
-                v |= (s * 4u * BB) << (8 * t);
+                const int step = 4 * wd + t;
+                int slot = 2 * (16 * (p & 1) + ((step + r) & 15)) + (nb ^ (p & 1));
+                slot ^= 32 * ((p >> 1) & 1);
+                v |= (uint32_t)(4 * slot) << (8 * t);
             }
-            offs[j][k] = v;
+            offs[nb][wd] = v;
         }
     }
+    uint32_t rgn[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) rgn[k] = (uint32_t)(((part + 16 * k) >> 1) << 4) * 0x01010101u;
+
+    float acc[kMaxRG];
+#pragma unroll
+    for (int g = 0; g < kMaxRG; ++g) acc[g] = 0.0f;
+
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
-
-    const int tiles = (a.N + kTileRows - 1) / kTileRows;
-    const int T0 = range * a.tiles_per_range;
-    const int T1 = imin(T0 + a.tiles_per_range, tiles);
-    for (int T = T0 + wave; T < T1; T += kThreads / 64) {
-        const int R = imin(kTileRows, a.N - kTileRows * T);
-        const bool active = lane < R;
-        const int n = kTileRows * T + lane;
-        float tot[BB];
+    const int jobs = a.B * pieces * nrg;  // (batch row, piece, row group), row group fastest
+    // activations of this thread's two table chunks (tid, tid + 256 of the piece)
+    auto load_x = [&](int b, int pc, uint4 xr[2]) {
 #pragma unroll
-        for (int bb = 0; bb < BB; ++bb) tot[bb] = 0.0f;
-
-        // all planes of this tile: keys and exponents
-        uint4 wv[SA_MAX_Q][GB];
-        int ev[SA_MAX_Q][GB];
+        for (int h = 0; h < 2; ++h) {
+            const int c = imin(kPieceChunks * pc + threadIdx.x + kThreads * h, C - 1);
+            xr[h] = *reinterpret_cast<const uint4*>(a.x + (int64_t)b * a.K + 8 * c);
+        }
+    };
+    // tables of piece pc for one batch row from this thread's two chunks
+    auto build = [&](const uint4 xr[2]) {
 #pragma unroll
-        for (int i = 0; i < SA_MAX_Q; ++i) {
-            if (i < a.q) {
-                const uint8_t* base =
-                    a.packed + ((int64_t)i * a.N + (int64_t)kTileRows * T) * C + 16 * lane;
-                const int8_t* erow = a.exps + ((int64_t)i * a.N + n) * NG;
+        for (int h = 0; h < 2; ++h) {
+            const int cr = threadIdx.x + kThreads * h;  // chunk within the piece
+            const int Jr = cr >> 4, u = cr & 15, rho = Jr >> 1, par = Jr & 1;
+            const uint32_t w4[4] = {xr[h].x, xr[h].y, xr[h].z, xr[h].w};
+            float f[8];
 #pragma unroll
-                for (int j = 0; j < GB; ++j) {
-                    if (j < nb && active) {
-                        wv[i][j] = *reinterpret_cast<const uint4*>(
-                            base + (int64_t)kBlockChunks * blk[j] * R);
-                        ev[i][j] = erow[blk[j] / bpg];
-                    } else {
-                        wv[i][j] = make_uint4(0, 0, 0, 0);
-                        ev[i][j] = 0;
-                    }
-                }
+            for (int t = 0; t < 4; ++t) {
+                f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
+                f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
             }
+            float lo[16], hi[16];
+            nibble_sums(f[0], f[1], f[2], f[3], lo);
+            nibble_sums(f[4], f[5], f[6], f[7], hi);
+            const int slot0 = (2 * (16 * par + u)) ^ (32 * (rho & 1));  // even slot of the pair
+            float2* dst = reinterpret_cast<float2*>(lut + rho * kRegionFloats + slot0);
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                dst[v * 32] = par ? make_float2(hi[v], lo[v]) : make_float2(lo[v], hi[v]);
         }
-#pragma unroll
-        for (int i = 0; i < SA_MAX_Q; ++i) {
-            if (i < a.q) {
-#pragma unroll
-                for (int j = 0; j < GB; ++j) {
-                    if (j < nb) {
-                        float acc[BB];
-#pragma unroll
-                        for (int bb = 0; bb < BB; ++bb) acc[bb] = 0.0f;
-                        const uint32_t words[4] = {wv[i][j].x, wv[i][j].y, wv[i][j].z, wv[i][j].w};
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-#pragma unroll
-                            for (int t = 0; t < 4; ++t) {
-                                // byte 0: slot offset (offs byte t); byte 1: key (word byte t)
-                                const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
-                                const uint32_t addr =
-                                    __builtin_amdgcn_perm(words[k], offs[j][k], sel);
-                                query_add<BB>(lut_bytes, addr, acc);
-                            }
-                        }
-#pragma unroll
-                        for (int bb = 0; bb < BB; ++bb) tot[bb] += ldexpf(acc[bb], ev[i][j]);
-                    }
-                }
-            }
-        }
+    };
 
-        if (a.k_slices == 1) {
-            if (active)
-                for (int bb = 0; bb < a.nbr; ++bb) a.y[(int64_t)bb * a.y_stride + n] = tot[bb];
-            continue;
+    // queries of one job, accumulation into its row group, and -- when the job
+    // completes batch row b -- the combination of the 16 lanes of every row
+    auto run_job = [&](int job, JobRegs<Q>& regs) {
+        const int g = job % nrg;
+        const int pc = (job / nrg) % pieces;
+        const int b = job / (nrg * pieces);
+        bool valid[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int Jr = part + 16 * k;
+            valid[k] = Jr < kPieceBlocks && kPieceBlocks * pc + Jr < C16;
         }
-        if (active)
-            for (int bb = 0; bb < a.nbr; ++bb)
-                a.partials[((int64_t)slice * BB + bb) * a.N + n] = tot[bb];
-        __threadfence();
-        unsigned ticket = 0;
-        if (lane == 0) ticket = atomicAdd(&a.tickets[T], 1u);
-        ticket = __shfl(ticket, 0);
-        if (ticket == (unsigned)(a.k_slices - 1)) {
-            __threadfence();
-            if (active) {
-                for (int bb = 0; bb < a.nbr; ++bb) {
-                    const float* src = a.partials + (int64_t)bb * a.N + n;
-                    float s = 0.0f;
-                    for (int sl = 0; sl < a.k_slices; ++sl)
-                        s += __builtin_nontemporal_load(src + (int64_t)sl * BB * a.N);
-                    a.y[(int64_t)bb * a.y_stride + n] = s;
+        const float v = job_sum<Q>(regs, valid, rgn, offs, lut_bytes);
+#pragma unroll
+        for (int gg = 0; gg < kMaxRG; ++gg)
+            if (gg == g) acc[gg] += v;
+        if (pc == pieces - 1 && g == nrg - 1) {
+#pragma unroll
+            for (int gg = 0; gg < kMaxRG; ++gg) {
+                if (gg < nrg) {
+                    float s = acc[gg];
+                    s += __shfl_xor(s, 16);
+                    s += __shfl_xor(s, 32);
+                    if (lane < kGroupRows) red[wave][kGroupRows * gg + r] = s;
                 }
+                acc[gg] = 0.0f;
             }
-            if (lane == 0) atomicExch(&a.tickets[T], 0u);
+            __syncthreads();
+            for (int t = threadIdx.x; t < kGroupRows * nrg; t += kThreads) {
+                const int n = kGroupRows * rg0 + t;
+                if (n < a.N)
+                    a.y[(int64_t)b * a.N + n] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
+            }
+            // red is written again only after the next batch row's table barriers
         }
+    };
+    auto load_job_n = [&](int job, JobRegs<Q>& regs) {
+        const int rg = rg0 + job % nrg, pc = (job / nrg) % pieces;
+        load_job_exps<Q>(a, rg, pc, part, r, C16, NG, bpg, regs);
+        load_job_keys<Q>(a, rg, pc, part, r, C, C16, regs);
+    };
+
+    // tables of the piece a job starts (between barriers)
+    auto start_piece = [&](int job) {
+        uint4 xr[2];
+        load_x(job / (nrg * pieces), (job / nrg) % pieces, xr);
+        __syncthreads();  // the previous piece's queries are done
+        __builtin_amdgcn_sched_barrier(0);
+        build(xr);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // Job 0: exponents, activations, then keys, so the first table build waits
+    // for the activations only while the keys stay in flight.
+    auto prologue = [&](JobRegs<Q>& j0) {
+        load_job_exps<Q>(a, rg0, 0, part, r, C16, NG, bpg, j0);
+        uint4 xr[2];
+        load_x(0, 0, xr);
+        load_job_keys<Q>(a, rg0, 0, part, r, C, C16, j0);
+        __builtin_amdgcn_sched_barrier(0);
+        build(xr);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    if (jobs == 1) {
+        JobRegs<Q> j0;
+        prologue(j0);
+        run_job(0, j0);
+        return;
+    }
+    // Several jobs: two register sets alternate (no copies of pending loads);
+    // each job's keys are requested before the previous job's queries.  The
+    // requests are unconditional -- past the last job they repeat it -- so no
+    // register set depends on a branch.
+    JobRegs<Q> j0, ja, jb;
+    prologue(j0);
+    load_job_n(1, ja);
+    run_job(0, j0);
+    for (int job = 1; job < jobs; job += 2) {
+        if (job % nrg == 0) start_piece(job);
+        load_job_n(imin(job + 1, jobs - 1), jb);
+        run_job(job, ja);
+        if (job + 1 >= jobs) break;
+        if ((job + 1) % nrg == 0) start_piece(job + 1);
+        load_job_n(imin(job + 2, jobs - 1), ja);
+        run_job(job + 1, jb);
     }
 }
 
@@ -424,115 +511,35 @@ int validate_gemm(const void* x, const void* packed, const void* exps, int q, in
     return SA_OK;
 }
 
-struct PassShape {
-    int gb, bb;
-};
-
-PassShape pass_shape(int rem) {
-    if (rem >= 3) return {1, 4};
-    if (rem == 2) return {2, 2};
-    return {2, 1};
+int rows_rg_per_wg(int N) {
+    // one row group (16 rows) per workgroup until the grid would exceed ~2
+    // workgroups per CU; beyond that a workgroup takes several row groups and
+    // reuses its tables across them
+    const int groups = (N + kGroupRows - 1) / kGroupRows;
+    int rg = groups / 512;
+    if (rg < 1) rg = 1;
+    if (rg > kMaxRG) rg = kMaxRG;
+    return rg;
 }
 
 void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     *p = sa_plan{};
     p->threads = kThreads;
-    const int tiles = (N + kTileRows - 1) / kTileRows;
     if (group % 128 != 0) {
         p->path = 0;
-        p->blocks_per_slice = (K / 8 + kBlockChunks - 1) / kBlockChunks;
-        p->batch_per_pass = 1;
-        p->passes = 1;
-        p->k_slices = 1;
-        p->row_ranges = (N + kThreads - 1) / kThreads;
-        p->rows_per_range = kThreads;
-        p->workgroups = p->row_ranges * batch;
+        p->rows_per_wg = kThreads;
+        p->workgroups = ((N + kThreads - 1) / kThreads) * batch;
+        p->pieces = (K / 8 + kBlockChunks - 1) / kBlockChunks;
         p->lds_bytes = sizeof(float) * (kBlockChunks * 256 + SA_MAX_Q * kThreads);
-        p->workspace_bytes = 0;
         return;
     }
-    const PassShape first = pass_shape(batch);
+    const int rg = rows_rg_per_wg(N);
+    const int groups = (N + kGroupRows - 1) / kGroupRows;
     p->path = 1;
-    p->blocks_per_slice = first.gb;
-    p->batch_per_pass = first.bb;
-    int passes = 0, rem = batch;
-    while (rem > 0) {
-        rem -= imin(rem, pass_shape(rem).bb);
-        ++passes;
-    }
-    p->passes = passes;
-    const int C16 = K / 128;
-    const int k_slices = (C16 + first.gb - 1) / first.gb;
-    const int waves = kThreads / 64;
-    const int ranges0 = (tiles + waves - 1) / waves;
-    // Give a workgroup more tiles (re-using its tables) once the grid would
-    // exceed ~2 workgroups per CU.
-    int per = (int)(((int64_t)ranges0 * k_slices) / 512);
-    if (per < 1) per = 1;
-    const int tiles_per_range = waves * per;
-    const int row_ranges = (tiles + tiles_per_range - 1) / tiles_per_range;
-    p->k_slices = k_slices;
-    p->row_ranges = row_ranges;
-    p->rows_per_range = tiles_per_range * kTileRows;
-    p->workgroups = row_ranges * k_slices;
-    p->lds_bytes = sizeof(float) * 256 * kKeyStride;
-    if (k_slices > 1)
-        p->workspace_bytes =
-            sizeof(unsigned) * (size_t)tiles + sizeof(float) * (size_t)k_slices * first.bb * N;
-}
-
-// Split-K workspace per (device, stream): a ticket array (one counter per
-// 64-row tile) and a partial-sum array, in separate buffers.  Tickets are
-// zeroed when their buffer is allocated and every call leaves them at zero;
-// nothing else is ever written to the ticket buffer.
-struct Workspace {
-    unsigned* tickets = nullptr;
-    size_t ticket_count = 0;
-    float* partials = nullptr;
-    size_t partial_bytes = 0;
-};
-std::mutex g_mu;
-std::map<std::pair<int, void*>, Workspace> g_ws;
-
-int get_workspace(void* stream, size_t tickets, size_t partial_bytes, unsigned** t_out,
-                  float** p_out) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
-    std::lock_guard<std::mutex> lock(g_mu);
-    Workspace& w = g_ws[{dev, stream}];
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const bool grow_t = w.ticket_count < tickets, grow_p = w.partial_bytes < partial_bytes;
-    if ((grow_t && w.tickets) || (grow_p && w.partials)) {
-        if (hipStreamSynchronize(s) != hipSuccess) return SA_ERR_HIP;
-    }
-    if (grow_t) {
-        if (w.tickets) (void)hipFree(w.tickets);
-        w.tickets = nullptr;
-        w.ticket_count = 0;
-        size_t want = tickets < 4096 ? 4096 : tickets;
-        void* p = nullptr;
-        if (hipMalloc(&p, want * sizeof(unsigned)) != hipSuccess) return SA_ERR_NOMEM;
-        if (hipMemsetAsync(p, 0, want * sizeof(unsigned), s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess) {
-            (void)hipFree(p);
-            return SA_ERR_HIP;
-        }
-        w.tickets = static_cast<unsigned*>(p);
-        w.ticket_count = want;
-    }
-    if (grow_p) {
-        if (w.partials) (void)hipFree(w.partials);
-        w.partials = nullptr;
-        w.partial_bytes = 0;
-        size_t want = partial_bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : partial_bytes;
-        void* p = nullptr;
-        if (hipMalloc(&p, want) != hipSuccess) return SA_ERR_NOMEM;
-        w.partials = static_cast<float*>(p);
-        w.partial_bytes = want;
-    }
-    *t_out = w.tickets;
-    *p_out = w.partials;
-    return SA_OK;
+    p->rows_per_wg = kGroupRows * rg;
+    p->workgroups = (groups + rg - 1) / rg;
+    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
+    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + (kThreads / 64) * kGroupRows * kMaxRG);
 }
 
 int launch_status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
@@ -544,9 +551,18 @@ int grid_for(int64_t items) {
     return (int)g;
 }
 
-template <int GB, int BB>
-void launch_splitk(const SplitKArgs& a, int workgroups, hipStream_t s) {
-    hipLaunchKernelGGL((k_gemm_splitk<GB, BB>), dim3(workgroups), dim3(kThreads), 0, s, a);
+void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
+    const dim3 g(workgroups), b(kThreads);
+    switch (q) {
+        case 1: hipLaunchKernelGGL(k_gemm_rows<1>, g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_gemm_rows<2>, g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(k_gemm_rows<3>, g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_gemm_rows<4>, g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(k_gemm_rows<5>, g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(k_gemm_rows<6>, g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(k_gemm_rows<7>, g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_gemm_rows<8>, g, b, 0, s, a); break;
+    }
 }
 
 }  // namespace
@@ -616,50 +632,24 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     sa_plan plan;
     make_plan(q, N, K, group, batch, &plan);
     if (plan.path == 0) {
-        hipLaunchKernelGGL(k_gemm_generic, dim3(plan.row_ranges, batch), dim3(kThreads), 0, s,
+        hipLaunchKernelGGL(k_gemm_generic, dim3((N + kThreads - 1) / kThreads, batch),
+                           dim3(kThreads), 0, s,
                            x, packed_bits, exps, q, N, K, group, y);
         return launch_status();
     }
-    const int tiles = (N + kTileRows - 1) / kTileRows;
-    unsigned* tickets = nullptr;
-    float* partials = nullptr;
-    if (plan.workspace_bytes > 0) {
-        const size_t pbytes = plan.workspace_bytes - sizeof(unsigned) * (size_t)tiles;
-        const int wst = get_workspace(stream, (size_t)tiles, pbytes, &tickets, &partials);
-        if (wst != SA_OK) return wst;
-    }
-    SplitKArgs a{};
-    a.x_stride = K;
+    RowsArgs a{};
+    a.x = x;
     a.packed = packed_bits;
     a.exps = exps;
     a.q = q;
     a.N = N;
     a.K = K;
     a.G = group;
-    a.y_stride = N;
-    a.tickets = tickets;
-    a.partials = partials;
-    a.row_ranges = plan.row_ranges;
-    a.tiles_per_range = plan.rows_per_range / kTileRows;
-    for (int b0 = 0; b0 < batch;) {
-        const PassShape ps = pass_shape(batch - b0);
-        const int nbr = imin(ps.bb, batch - b0);
-        a.x = x + (int64_t)b0 * K;
-        a.y = y + (int64_t)b0 * N;
-        a.nbr = nbr;
-        a.k_slices = (K / 128 + ps.gb - 1) / ps.gb;
-        const int wgs = plan.row_ranges * a.k_slices;
-        if (ps.bb == 4)
-            launch_splitk<1, 4>(a, wgs, s);
-        else if (ps.bb == 2)
-            launch_splitk<2, 2>(a, wgs, s);
-        else
-            launch_splitk<2, 1>(a, wgs, s);
-        const int lst = launch_status();
-        if (lst != SA_OK) return lst;
-        b0 += nbr;
-    }
-    return SA_OK;
+    a.B = batch;
+    a.y = y;
+    a.rg_per_wg = plan.rows_per_wg / kGroupRows;
+    launch_rows(q, a, plan.workgroups, s);
+    return launch_status();
 }
 
 SA_API const char* sa_status_string(int status) {
@@ -671,25 +661,10 @@ SA_API const char* sa_status_string(int status) {
         case SA_ERR_GROUP: return "group must be a multiple of 8 that divides K";
         case SA_ERR_ALIGN: return "x, packed_bits, y and lut must be 16-byte aligned";
         case SA_ERR_HIP: return "HIP runtime error or kernel launch failure";
-        case SA_ERR_NOMEM: return "could not allocate the split-K workspace";
         default: return "unknown status";
     }
 }
 
 SA_API const char* sa_version(void) { return SA_VERSION_STRING; }
-
-SA_API void sa_shutdown(void) {
-    std::lock_guard<std::mutex> lock(g_mu);
-    int cur = 0;
-    (void)hipGetDevice(&cur);
-    for (auto& kv : g_ws) {
-        (void)hipSetDevice(kv.first.first);
-        (void)hipStreamSynchronize(reinterpret_cast<hipStream_t>(kv.first.second));
-        if (kv.second.tickets) (void)hipFree(kv.second.tickets);
-        if (kv.second.partials) (void)hipFree(kv.second.partials);
-    }
-    (void)hipSetDevice(cur);
-    g_ws.clear();
-}
 
 }  // extern "C"

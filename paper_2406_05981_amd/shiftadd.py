@@ -26,16 +26,11 @@ if not os.path.exists(LIB_PATH):
 class SaPlan(ctypes.Structure):
     _fields_ = [
         ("path", ctypes.c_int),
-        ("blocks_per_slice", ctypes.c_int),
-        ("batch_per_pass", ctypes.c_int),
-        ("passes", ctypes.c_int),
-        ("k_slices", ctypes.c_int),
-        ("row_ranges", ctypes.c_int),
-        ("rows_per_range", ctypes.c_int),
+        ("rows_per_wg", ctypes.c_int),
         ("workgroups", ctypes.c_int),
         ("threads", ctypes.c_int),
+        ("pieces", ctypes.c_int),
         ("lds_bytes", ctypes.c_size_t),
-        ("workspace_bytes", ctypes.c_size_t),
     ]
 
 
@@ -52,7 +47,6 @@ def _bind(lib):
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_status_string": ([I], ctypes.c_char_p),
         "sa_version": ([], ctypes.c_char_p),
-        "sa_shutdown": ([], None),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -63,8 +57,8 @@ def _bind(lib):
 
 lib = _bind(ctypes.CDLL(LIB_PATH))
 
-SA_OK, SA_ERR_NULL, SA_ERR_SHAPE, SA_ERR_Q, SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_HIP, SA_ERR_NOMEM = (
-    0, -1, -2, -3, -4, -5, -6, -7)
+SA_OK, SA_ERR_NULL, SA_ERR_SHAPE, SA_ERR_Q, SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_HIP = (
+    0, -1, -2, -3, -4, -5, -6)
 SA_MAX_Q = 8
 SA_MAX_BATCH = 256
 
@@ -108,10 +102,6 @@ def sa_status_string(status: int) -> str:
 
 def sa_version() -> str:
     return lib.sa_version().decode()
-
-
-def sa_shutdown() -> None:
-    lib.sa_shutdown()
 
 
 def sa_packed_bytes(q: int, N: int, K: int) -> int:

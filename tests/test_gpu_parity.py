@@ -236,10 +236,10 @@ def test_non_default_stream():
     check(y, y_ref, a_ref, "side stream")
 
 
-def test_workspace_reuse_across_shapes():
-    """Alternating shapes with different split-K geometry on one stream: every
-    call must leave the tile tickets at zero for the next."""
-    say("workspace reuse")
+def test_alternating_shapes_on_one_stream():
+    """Alternating shapes with different launch geometry (pieces, batch) on one
+    stream: no call may depend on state left by another."""
+    say("alternating shapes")
     cases = [workloads.random_case(3, 300, 4096, 128, 1, seed=10),
              workloads.random_case(2, 1000, 11008, 128, 2, seed=11),
              workloads.random_case(3, 300, 4096, 128, 5, seed=12)]
@@ -288,11 +288,10 @@ def test_binding_raises_on_bad_arguments():
         sa.sa_shiftadd_gemm(x, packed, e, 3, 64, 256, 96, 1, ybig[:64])
 
 
-def test_tickets_survive_smaller_earlier_calls():
-    """Regression: a call with few 64-row tiles and large partial sums, followed
-    by a call with more tiles on the same stream.  The second call's tile
-    tickets must not alias the first call's partial sums."""
-    say("ticket aliasing regression")
+def test_small_then_large_row_counts():
+    """Regression (an earlier design kept per-tile state between calls): a call
+    with few rows and a large batch, then one with many rows, alternately."""
+    say("small then large row counts")
     first = workloads.random_case(2, 1000, 4096, 128, 16, seed=16)
     second = workloads.random_case(3, 4097, 512, 128, 1, seed=17)
     for c in (first, second, first, second):
