@@ -206,22 +206,26 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
 // odd block -> 32 + (2u+1, 2u) (swapped), odd regions -> slot ^ 32.
 //
 // Work split.  Row r of a 16-row group is handled by lanes r, r+16, r+32,
-// r+48 of all four waves: part = 4*wave + (lane >> 4) owns the blocks
-// J = part + 16k of each piece.  Keys are stored rotated by row (position t of
-// a row's 16 bytes holds chunk (t + row) mod 16), so at each query the 32
-// lanes of a half-wave touch 32 different slots mod 32 (and the 64 lanes 64
-// different slots mod 64): no LDS bank conflicts by construction.
+// r+48 of all eight waves: part = 4*wave + (lane >> 4) owns block `part` of
+// each piece.  Keys are stored rotated by row (position t of a row's 16 bytes
+// holds chunk (t + row) mod 16), so at each query the 32 lanes of a half-wave
+// touch 32 different slots mod 32 (and the 64 lanes 64 different slots mod
+// 64): no LDS bank conflicts by construction.
 //
-// Each lane adds the 32 half-entries of one block, shifts the sum by the
-// block's exponent (ldexp) and accumulates in fp32; the 16 lanes of a row are
-// then combined in a fixed order (two xor-shuffles, then the four waves via
+// Each lane adds the 32 half-entries of its block, shifts the sum by the
+// block's exponent (ldexp) and accumulates in fp32; the 32 lanes of a row are
+// then combined in a fixed order (two xor-shuffles, then the eight waves via
 // LDS).  The result is deterministic.
 
+constexpr int kRowThreads = 512;     // 8 waves: 2 per SIMD
+constexpr int kRowWaves = kRowThreads / 64;
 constexpr int kGroupRows = 16;       // rows per row group
 constexpr int kPieceBlocks = 32;     // 128-column blocks per table piece (4096 columns)
 constexpr int kPieceChunks = kPieceBlocks * kBlockChunks;
 constexpr int kRegionFloats = 1024;  // 4 KB: 16 values x 64 slots
 constexpr int kMaxRG = 8;            // row groups per workgroup
+static_assert(kRowThreads == kPieceChunks, "one table chunk per thread");
+static_assert(4 * kRowWaves == kPieceBlocks, "one block per lane per piece");
 
 struct RowsArgs {
     const uint16_t* x;  // activations [B][K]
@@ -232,48 +236,34 @@ struct RowsArgs {
     int rg_per_wg;      // row groups per workgroup (<= kMaxRG)
 };
 
-// Keys and exponents of one (row group, piece) job for this lane: Q planes x 2 blocks.
+// Keys and exponents of one (row group, piece) job for this lane: Q planes of
+// one block.
 template <int Q>
 struct JobRegs {
-    uint4 w[Q][2];
-    int e[Q][2];  // exponent (sign-extending byte load)
+    uint4 w[Q];
+    int e[Q];  // exponent (sign-extending byte load)
 };
 
 // Exponents are requested before keys (and, for the first job, before the
 // activations): whatever the compiler hoists onto the exponents then waits for
 // them alone, never for the keys behind them.
 template <int Q>
-__device__ inline void load_job_exps(const RowsArgs& a, int rg, int pc, int part, int r, int C16,
-                                     int NG, int bpg, JobRegs<Q>& j) {
-    const int n = imin(kGroupRows * rg + r, a.N - 1);
-    const int8_t* erow_base = a.exps + (int64_t)n * NG;
+__device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, int bpg,
+                                     JobRegs<Q>& j) {
+    const int8_t* erow = a.exps + (int64_t)n * NG + J / bpg;
 #pragma unroll
-    for (int i = 0; i < Q; ++i) {
-        const int8_t* erow = erow_base + (int64_t)i * a.N * NG;
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const int J = imin(kPieceBlocks * pc + part + 16 * k, C16 - 1);
-            j.e[i][k] = erow[J / bpg];
-        }
-    }
+    for (int i = 0; i < Q; ++i) j.e[i] = erow[(int64_t)i * a.N * NG];
 }
 
 template <int Q>
-__device__ inline void load_job_keys(const RowsArgs& a, int rg, int pc, int part, int r, int C,
-                                     int C16, JobRegs<Q>& j) {
-    const int n = imin(kGroupRows * rg + r, a.N - 1);
+__device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, JobRegs<Q>& j) {
     const int T = n >> 6;
     const int R = imin(kTileRows, a.N - kTileRows * T);
+    const uint8_t* base = a.packed + (int64_t)kTileRows * T * C + 16 * (n & 63) +
+                          (int64_t)kBlockChunks * J * R;
 #pragma unroll
-    for (int i = 0; i < Q; ++i) {
-        const uint8_t* base =
-            a.packed + ((int64_t)i * a.N + (int64_t)kTileRows * T) * C + 16 * (n & 63);
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const int J = imin(kPieceBlocks * pc + part + 16 * k, C16 - 1);
-            j.w[i][k] = *reinterpret_cast<const uint4*>(base + (int64_t)kBlockChunks * J * R);
-        }
-    }
+    for (int i = 0; i < Q; ++i)
+        j.w[i] = *reinterpret_cast<const uint4*>(base + (int64_t)i * a.N * C);
 }
 
 // Empty asm that "may modify" one plane's job registers: their consumers
@@ -281,53 +271,47 @@ __device__ inline void load_job_keys(const RowsArgs& a, int rg, int pc, int part
 // here -- after the tables are built and after the previous plane's queries.
 template <int Q>
 __device__ inline void pin_plane(JobRegs<Q>& j, int i) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k)
-        asm volatile("" : "+v"(j.w[i][k].x), "+v"(j.w[i][k].y), "+v"(j.w[i][k].z),
-                     "+v"(j.w[i][k].w), "+v"(j.e[i][k]));
+    asm volatile("" : "+v"(j.w[i].x), "+v"(j.w[i].y), "+v"(j.w[i].z), "+v"(j.w[i].w),
+                 "+v"(j.e[i]));
 }
 
-// Queries and adds of one job; returns sum over planes and owned blocks of
-// ldexp(block sum, exponent).  Planes are consumed in load order, so a plane's
-// queries run while later planes are still arriving.
+// Queries and adds of one job: sum over planes of ldexp(block sum, exponent).
+// Planes are consumed in load order, so a plane's queries run while later
+// planes are still arriving.
 template <int Q>
-__device__ inline float job_sum(JobRegs<Q>& j, const bool valid[2], const uint32_t rgn[2],
-                                const uint32_t offs[2][4], const char* lut_bytes) {
+__device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn, const uint32_t offs[2][4],
+                                const char* lut_bytes) {
     float tot = 0.0f;
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
         __builtin_amdgcn_sched_barrier(0);
         pin_plane<Q>(j, i);
+        const uint32_t words[4] = {j.w[i].x, j.w[i].y, j.w[i].z, j.w[i].w};
+        float acc = 0.0f;
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const uint32_t words[4] = {j.w[i][k].x, j.w[i][k].y, j.w[i][k].z, j.w[i][k].w};
-            float acc = 0.0f;
+        for (int wd = 0; wd < 4; ++wd) {
+            // key nibbles of 4 bytes, each or'ed with this block's region
+            const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn;
+            const uint32_t hi = ((words[wd] >> 4) & 0x0f0f0f0fu) | rgn;
 #pragma unroll
-            for (int wd = 0; wd < 4; ++wd) {
-                // key nibbles of 4 bytes, each or'ed with this block's region
-                const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn[k];
-                const uint32_t hi = ((words[wd] >> 4) & 0x0f0f0f0fu) | rgn[k];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    // byte 0: slot offset (offs byte t); byte 1: region|nibble (byte t)
-                    const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
-                    acc += *reinterpret_cast<const float*>(
-                        lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
-                    acc += *reinterpret_cast<const float*>(
-                        lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
-                }
+            for (int t = 0; t < 4; ++t) {
+                // byte 0: slot offset (offs byte t); byte 1: region|nibble (byte t)
+                const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                acc += *reinterpret_cast<const float*>(
+                    lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
+                acc += *reinterpret_cast<const float*>(
+                    lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
             }
-            const float v = ldexpf(acc, j.e[i][k]);
-            tot += valid[k] ? v : 0.0f;
         }
+        tot += ldexpf(acc, j.e[i]);
     }
     return tot;
 }
 
 template <int Q>
-__global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
+__global__ __launch_bounds__(kRowThreads) void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kThreads / 64][kGroupRows * kMaxRG];
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
@@ -337,8 +321,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
     const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
 
     // Slot offsets of this lane's 16 key positions, low and high nibble (4
-    // positions per register, one per byte), and the region bits of its two
-    // blocks, replicated in every byte's high nibble.
+    // positions per register, one per byte), and the region bits of its block,
+    // replicated in every byte's high nibble.
     uint32_t offs[2][4];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -355,9 +339,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
             offs[nb][wd] = v;
         }
     }
-    uint32_t rgn[2];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) rgn[k] = (uint32_t)(((part + 16 * k) >> 1) << 4) * 0x01010101u;
+    const uint32_t rgn = (uint32_t)((part >> 1) << 4) * 0x01010101u;
 
     float acc[kMaxRG];
 #pragma unroll
@@ -365,54 +347,46 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
 
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
     const int jobs = a.B * pieces * nrg;  // (batch row, piece, row group), row group fastest
-    // activations of this thread's two table chunks (tid, tid + 256 of the piece)
-    auto load_x = [&](int b, int pc, uint4 xr[2]) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int c = imin(kPieceChunks * pc + threadIdx.x + kThreads * h, C - 1);
-            xr[h] = *reinterpret_cast<const uint4*>(a.x + (int64_t)b * a.K + 8 * c);
-        }
+    auto job_row = [&](int job) { return imin(kGroupRows * (rg0 + job % nrg) + r, a.N - 1); };
+    auto job_block = [&](int job) {
+        return imin(kPieceBlocks * ((job / nrg) % pieces) + part, C16 - 1);
     };
-    // tables of piece pc for one batch row from this thread's two chunks
-    auto build = [&](const uint4 xr[2]) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int cr = threadIdx.x + kThreads * h;  // chunk within the piece
-            const int Jr = cr >> 4, u = cr & 15, rho = Jr >> 1, par = Jr & 1;
-            const uint32_t w4[4] = {xr[h].x, xr[h].y, xr[h].z, xr[h].w};
-            float f[8];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
-                f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
-            }
-            float lo[16], hi[16];
-            nibble_sums(f[0], f[1], f[2], f[3], lo);
-            nibble_sums(f[4], f[5], f[6], f[7], hi);
-            const int slot0 = (2 * (16 * par + u)) ^ (32 * (rho & 1));  // even slot of the pair
-            float2* dst = reinterpret_cast<float2*>(lut + rho * kRegionFloats + slot0);
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-                dst[v * 32] = par ? make_float2(hi[v], lo[v]) : make_float2(lo[v], hi[v]);
-        }
+    // activations of this thread's table chunk (chunk tid of the piece)
+    auto load_x = [&](int b, int pc) {
+        const int c = imin(kPieceChunks * pc + (int)threadIdx.x, C - 1);
+        return *reinterpret_cast<const uint4*>(a.x + (int64_t)b * a.K + 8 * c);
     };
-
+    // tables of one piece for one batch row from this thread's chunk
+    auto build = [&](const uint4 xr) {
+        const int cr = threadIdx.x;  // chunk within the piece
+        const int Jr = cr >> 4, u = cr & 15, rho = Jr >> 1, par = Jr & 1;
+        const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
+        float f[8];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
+            f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
+        }
+        float lo[16], hi[16];
+        nibble_sums(f[0], f[1], f[2], f[3], lo);
+        nibble_sums(f[4], f[5], f[6], f[7], hi);
+        const int slot0 = (2 * (16 * par + u)) ^ (32 * (rho & 1));  // even slot of the pair
+        float2* dst = reinterpret_cast<float2*>(lut + rho * kRegionFloats + slot0);
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            dst[v * 32] = par ? make_float2(hi[v], lo[v]) : make_float2(lo[v], hi[v]);
+    };
     // queries of one job, accumulation into its row group, and -- when the job
-    // completes batch row b -- the combination of the 16 lanes of every row
+    // completes batch row b -- the combination of the 32 lanes of every row
     auto run_job = [&](int job, JobRegs<Q>& regs) {
         const int g = job % nrg;
         const int pc = (job / nrg) % pieces;
         const int b = job / (nrg * pieces);
-        bool valid[2];
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const int Jr = part + 16 * k;
-            valid[k] = Jr < kPieceBlocks && kPieceBlocks * pc + Jr < C16;
-        }
-        const float v = job_sum<Q>(regs, valid, rgn, offs, lut_bytes);
+        const bool valid = kPieceBlocks * pc + part < C16;
+        const float v = job_sum<Q>(regs, rgn, offs, lut_bytes);
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
-            if (gg == g) acc[gg] += v;
+            if (gg == g && valid) acc[gg] += v;
         if (pc == pieces - 1 && g == nrg - 1) {
 #pragma unroll
             for (int gg = 0; gg < kMaxRG; ++gg) {
@@ -425,38 +399,38 @@ __global__ __launch_bounds__(kThreads) void k_gemm_rows(RowsArgs a) {
                 acc[gg] = 0.0f;
             }
             __syncthreads();
-            for (int t = threadIdx.x; t < kGroupRows * nrg; t += kThreads) {
+            for (int t = threadIdx.x; t < kGroupRows * nrg; t += kRowThreads) {
                 const int n = kGroupRows * rg0 + t;
-                if (n < a.N)
-                    a.y[(int64_t)b * a.N + n] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
+                if (n < a.N) {
+                    float s = red[0][t];
+#pragma unroll
+                    for (int w = 1; w < kRowWaves; ++w) s += red[w][t];
+                    a.y[(int64_t)b * a.N + n] = s;
+                }
             }
             // red is written again only after the next batch row's table barriers
         }
     };
     auto load_job_n = [&](int job, JobRegs<Q>& regs) {
-        const int rg = rg0 + job % nrg, pc = (job / nrg) % pieces;
-        load_job_exps<Q>(a, rg, pc, part, r, C16, NG, bpg, regs);
-        load_job_keys<Q>(a, rg, pc, part, r, C, C16, regs);
+        const int n = job_row(job), J = job_block(job);
+        load_job_exps<Q>(a, n, J, NG, bpg, regs);
+        load_job_keys<Q>(a, n, J, C, regs);
     };
-
     // tables of the piece a job starts (between barriers)
     auto start_piece = [&](int job) {
-        uint4 xr[2];
-        load_x(job / (nrg * pieces), (job / nrg) % pieces, xr);
+        const uint4 xr = load_x(job / (nrg * pieces), (job / nrg) % pieces);
         __syncthreads();  // the previous piece's queries are done
         __builtin_amdgcn_sched_barrier(0);
         build(xr);
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
     };
-
     // Job 0: exponents, activations, then keys, so the first table build waits
     // for the activations only while the keys stay in flight.
     auto prologue = [&](JobRegs<Q>& j0) {
-        load_job_exps<Q>(a, rg0, 0, part, r, C16, NG, bpg, j0);
-        uint4 xr[2];
-        load_x(0, 0, xr);
-        load_job_keys<Q>(a, rg0, 0, part, r, C, C16, j0);
+        load_job_exps<Q>(a, job_row(0), job_block(0), NG, bpg, j0);
+        const uint4 xr = load_x(0, 0);
+        load_job_keys<Q>(a, job_row(0), job_block(0), C, j0);
         __builtin_amdgcn_sched_barrier(0);
         build(xr);
         __syncthreads();
@@ -539,7 +513,8 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     p->rows_per_wg = kGroupRows * rg;
     p->workgroups = (groups + rg - 1) / rg;
     p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
-    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + (kThreads / 64) * kGroupRows * kMaxRG);
+    p->threads = kRowThreads;
+    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
 int launch_status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
@@ -552,7 +527,7 @@ int grid_for(int64_t items) {
 }
 
 void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
-    const dim3 g(workgroups), b(kThreads);
+    const dim3 g(workgroups), b(kRowThreads);
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows<2>, g, b, 0, s, a); break;
