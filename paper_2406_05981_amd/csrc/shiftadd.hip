@@ -223,7 +223,7 @@ constexpr int kGroupRows = 16;       // rows per row group
 constexpr int kPieceBlocks = 32;     // 128-column blocks per table piece (4096 columns)
 constexpr int kPieceChunks = kPieceBlocks * kBlockChunks;
 constexpr int kRegionFloats = 1024;  // 4 KB: 16 values x 64 slots
-constexpr int kMaxRG = 8;            // row groups per workgroup
+constexpr int kMaxRG = 4;            // row groups per workgroup
 static_assert(kRowThreads == kPieceChunks, "one table chunk per thread");
 static_assert(4 * kRowWaves == kPieceBlocks, "one block per lane per piece");
 
@@ -309,9 +309,8 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn, const uint32_t offs
 }
 
 template <int Q>
-__global__ __launch_bounds__(kRowThreads) void k_gemm_rows(RowsArgs a) {
-    __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+__device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
+                                               float (*red)[kGroupRows * kMaxRG]) {
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
@@ -447,12 +446,10 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows(RowsArgs a) {
     // each job's keys are requested before the previous job's queries.  The
     // requests are unconditional -- past the last job they repeat it -- so no
     // register set depends on a branch.
-    JobRegs<Q> j0, ja, jb;
-    prologue(j0);
-    load_job_n(1, ja);
-    run_job(0, j0);
-    for (int job = 1; job < jobs; job += 2) {
-        if (job % nrg == 0) start_piece(job);
+    JobRegs<Q> ja, jb;
+    prologue(ja);
+    for (int job = 0; job < jobs; job += 2) {
+        if (job > 0 && job % nrg == 0) start_piece(job);
         load_job_n(imin(job + 1, jobs - 1), jb);
         run_job(job, ja);
         if (job + 1 >= jobs) break;
@@ -461,6 +458,25 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows(RowsArgs a) {
         run_job(job + 1, jb);
     }
 }
+
+// Up to 4 planes: two 8-wave workgroups per CU (4 waves per SIMD, <= 128
+// VGPRs).  More planes need more registers: one workgroup per CU.
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_gemm_rows(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q>(a, lut, red);
+}
+
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q>(a, lut, red);
+}
+
+constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
 
 // ---------------------------------------------------------------- host side
 
@@ -485,12 +501,13 @@ int validate_gemm(const void* x, const void* packed, const void* exps, int q, in
     return SA_OK;
 }
 
-int rows_rg_per_wg(int N) {
-    // one row group (16 rows) per workgroup until the grid would exceed ~2
-    // workgroups per CU; beyond that a workgroup takes several row groups and
-    // reuses its tables across them
+int rows_rg_per_wg(int q, int N) {
+    // As many workgroups as are resident at once (two per CU up to 3 planes,
+    // one beyond), every workgroup taking a contiguous range of 16-row groups
+    // and reusing its tables across them.
+    const int resident = q <= kRowsResidentQ ? 512 : 256;
     const int groups = (N + kGroupRows - 1) / kGroupRows;
-    int rg = groups / 512;
+    int rg = (groups + resident - 1) / resident;
     if (rg < 1) rg = 1;
     if (rg > kMaxRG) rg = kMaxRG;
     return rg;
@@ -507,7 +524,7 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
         p->lds_bytes = sizeof(float) * (kBlockChunks * 256 + SA_MAX_Q * kThreads);
         return;
     }
-    const int rg = rows_rg_per_wg(N);
+    const int rg = rows_rg_per_wg(q, N);
     const int groups = (N + kGroupRows - 1) / kGroupRows;
     p->path = 1;
     p->rows_per_wg = kGroupRows * rg;
@@ -533,10 +550,10 @@ void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
         case 2: hipLaunchKernelGGL(k_gemm_rows<2>, g, b, 0, s, a); break;
         case 3: hipLaunchKernelGGL(k_gemm_rows<3>, g, b, 0, s, a); break;
         case 4: hipLaunchKernelGGL(k_gemm_rows<4>, g, b, 0, s, a); break;
-        case 5: hipLaunchKernelGGL(k_gemm_rows<5>, g, b, 0, s, a); break;
-        case 6: hipLaunchKernelGGL(k_gemm_rows<6>, g, b, 0, s, a); break;
-        case 7: hipLaunchKernelGGL(k_gemm_rows<7>, g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL(k_gemm_rows<8>, g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(k_gemm_rows_wide<5>, g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(k_gemm_rows_wide<6>, g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(k_gemm_rows_wide<7>, g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_gemm_rows_wide<8>, g, b, 0, s, a); break;
     }
 }
 
