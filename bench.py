@@ -51,10 +51,11 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, batch: int):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, or None
-    when none matches the current kernel source."""
-    path = os.path.join(PROFILES, f"traffic_{workload}_b{batch}.md")
+def measured_traffic(workload: str, layer: int, batch: int):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    workload (FETCH_SIZE and WRITE_SIZE scaled by a plain copy kernel), or None
+    when there is none or it was taken on a different kernel source."""
+    path = os.path.join(PROFILES, f"k_gemm_rows_{workload}_l{layer}_b{batch}.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"TRAFFIC_JSON:\s*(\{.*\})", open(path).read())
@@ -221,7 +222,7 @@ def main() -> int:
     log(f"{args.steps} steps in {ms:.3f} ms: {us_layer:.3f} us/layer, {gbs:.1f} GB/s "
         f"({100 * gbs / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f} GB/s)")
 
-    traffic = measured_traffic(args.workload, B)
+    traffic = measured_traffic(args.workload, args.layer, B)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
