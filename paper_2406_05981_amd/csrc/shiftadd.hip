@@ -58,8 +58,9 @@ __device__ inline void load_chunk(const uint16_t* p, float f[8]) {
 // out[a] = (+-x0 +-x1) + (+-x2 +-x3).  Flipping every bit of a negates the
 // result exactly, so table entries m and 255-m are exact negatives.
 __device__ inline void nibble_sums(float x0, float x1, float x2, float x3, float out[16]) {
-    const float p01[4] = {-x0 - x1, x0 - x1, x1 - x0, x0 + x1};
-    const float p23[4] = {-x2 - x3, x2 - x3, x3 - x2, x2 + x3};
+    const float s01 = x0 + x1, d01 = x0 - x1, s23 = x2 + x3, d23 = x2 - x3;
+    const float p01[4] = {-s01, d01, -d01, s01};
+    const float p23[4] = {-s23, d23, -d23, s23};
 #pragma unroll
     for (int a = 0; a < 16; ++a) out[a] = p01[a & 3] + p23[a >> 2];
 }
@@ -250,7 +251,7 @@ struct JobRegs {
 template <int Q>
 __device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, int bpg,
                                      JobRegs<Q>& j) {
-    const int8_t* erow = a.exps + (int64_t)n * NG + J / bpg;
+    const int8_t* erow = a.exps + (int64_t)n * NG + (bpg == 1 ? J : J / bpg);
 #pragma unroll
     for (int i = 0; i < Q; ++i) j.e[i] = erow[(int64_t)i * a.N * NG];
 }
@@ -321,21 +322,21 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 
     // Slot offsets of this lane's 16 key positions, low and high nibble (4
     // positions per register, one per byte), and the region bits of its block,
-    // replicated in every byte's high nibble.
+    // replicated in every byte's high nibble.  Byte t of offs[nb][wd] is
+    // 4*slot for position 4*wd+t:
+    //   slot = 2*(16*(p&1) + ((pos + r) & 15)) + (nb ^ (p&1)), xor 32 if (p>>1)&1
+    // i.e. 8*((pos + r) & 15) + 4*(nb ^ (p&1)) + 128*((p ^ (p>>1)) & 1).
     uint32_t offs[2][4];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    {
+        const uint32_t hi_bit = (uint32_t)(((p ^ (p >> 1)) & 1) << 7) * 0x01010101u;
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
-            uint32_t v = 0;
+            // 8*((4*wd + t + r) & 15) for t = 0..3, one per byte
+            const uint32_t base = (uint32_t)(((4 * wd + r) & 15) * 8) * 0x01010101u;
+            const uint32_t steps = (base + 0x18100800u) & 0x78787878u;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int step = 4 * wd + t;
-                int slot = 2 * (16 * (p & 1) + ((step + r) & 15)) + (nb ^ (p & 1));
-                slot ^= 32 * ((p >> 1) & 1);
-                v |= (uint32_t)(4 * slot) << (8 * t);
-            }
-            offs[nb][wd] = v;
+            for (int nb = 0; nb < 2; ++nb)
+                offs[nb][wd] = steps | hi_bit | ((uint32_t)((nb ^ (p & 1)) << 2) * 0x01010101u);
         }
     }
     const uint32_t rgn = (uint32_t)((part >> 1) << 4) * 0x01010101u;
@@ -350,15 +351,20 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     auto job_block = [&](int job) {
         return imin(kPieceBlocks * ((job / nrg) % pieces) + part, C16 - 1);
     };
-    // activations of this thread's table chunk (chunk tid of the piece)
+    // Tables are wave-local: the 64 lanes of a wave build the 64 chunks of the
+    // four blocks that wave queries (lane (r, p) builds chunk r of block
+    // `part`), so no table write is ever read by another wave and the only
+    // workgroup barrier is the final combination of the waves' row sums.
+    const int my_rho = part >> 1;
+    const int slot_lo = ((2 * (16 * (p & 1) + r)) + (p & 1)) ^ (32 * ((p >> 1) & 1));
+    const int slot_hi = slot_lo ^ 1;
+    // activations of this lane's table chunk
     auto load_x = [&](int b, int pc) {
-        const int c = imin(kPieceChunks * pc + (int)threadIdx.x, C - 1);
+        const int c = imin(kPieceChunks * pc + kBlockChunks * part + r, C - 1);
         return *reinterpret_cast<const uint4*>(a.x + (int64_t)b * a.K + 8 * c);
     };
-    // tables of one piece for one batch row from this thread's chunk
+    // tables of this wave's four blocks of one piece for one batch row
     auto build = [&](const uint4 xr) {
-        const int cr = threadIdx.x;  // chunk within the piece
-        const int Jr = cr >> 4, u = cr & 15, rho = Jr >> 1, par = Jr & 1;
         const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
         float f[8];
 #pragma unroll
@@ -369,11 +375,17 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         float lo[16], hi[16];
         nibble_sums(f[0], f[1], f[2], f[3], lo);
         nibble_sums(f[4], f[5], f[6], f[7], hi);
-        const int slot0 = (2 * (16 * par + u)) ^ (32 * (rho & 1));  // even slot of the pair
-        float2* dst = reinterpret_cast<float2*>(lut + rho * kRegionFloats + slot0);
+        float* t_lo = lut + my_rho * kRegionFloats + slot_lo;
+        float* t_hi = lut + my_rho * kRegionFloats + slot_hi;
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            dst[v * 32] = par ? make_float2(hi[v], lo[v]) : make_float2(lo[v], hi[v]);
+        for (int v = 0; v < 16; ++v) {
+            t_lo[v * 64] = lo[v];
+            t_hi[v * 64] = hi[v];
+        }
+        // the wave's own queries follow; LDS accesses of one wave complete in order
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
     // queries of one job, accumulation into its row group, and -- when the job
     // completes batch row b -- the combination of the 32 lanes of every row
@@ -407,22 +419,13 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                     a.y[(int64_t)b * a.N + n] = s;
                 }
             }
-            // red is written again only after the next batch row's table barriers
+            __syncthreads();  // red is rewritten by the next batch row
         }
     };
     auto load_job_n = [&](int job, JobRegs<Q>& regs) {
         const int n = job_row(job), J = job_block(job);
         load_job_exps<Q>(a, n, J, NG, bpg, regs);
         load_job_keys<Q>(a, n, J, C, regs);
-    };
-    // tables of the piece a job starts (between barriers)
-    auto start_piece = [&](int job) {
-        const uint4 xr = load_x(job / (nrg * pieces), (job / nrg) % pieces);
-        __syncthreads();  // the previous piece's queries are done
-        __builtin_amdgcn_sched_barrier(0);
-        build(xr);
-        __syncthreads();
-        __builtin_amdgcn_sched_barrier(0);
     };
     // Job 0: exponents, activations, then keys, so the first table build waits
     // for the activations only while the keys stay in flight.
@@ -432,7 +435,6 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         load_job_keys<Q>(a, job_row(0), job_block(0), C, j0);
         __builtin_amdgcn_sched_barrier(0);
         build(xr);
-        __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
     };
 
@@ -443,17 +445,19 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         return;
     }
     // Several jobs: two register sets alternate (no copies of pending loads);
-    // each job's keys are requested before the previous job's queries.  The
-    // requests are unconditional -- past the last job they repeat it -- so no
-    // register set depends on a branch.
+    // each job's keys (and, when it starts a piece, its activations) are
+    // requested before the previous job's queries.  The key requests are
+    // unconditional -- past the last job they repeat it -- so no register set
+    // depends on a branch.
     JobRegs<Q> ja, jb;
     prologue(ja);
     for (int job = 0; job < jobs; job += 2) {
-        if (job > 0 && job % nrg == 0) start_piece(job);
+        if (job > 0 && job % nrg == 0) build(load_x(job / (nrg * pieces), (job / nrg) % pieces));
         load_job_n(imin(job + 1, jobs - 1), jb);
         run_job(job, ja);
         if (job + 1 >= jobs) break;
-        if ((job + 1) % nrg == 0) start_piece(job + 1);
+        if ((job + 1) % nrg == 0)
+            build(load_x((job + 1) / (nrg * pieces), ((job + 1) / nrg) % pieces));
         load_job_n(imin(job + 2, jobs - 1), ja);
         run_job(job + 1, jb);
     }
