@@ -51,11 +51,14 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, layer: int, batch: int):
+KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch"}
+
+
+def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this
     workload (FETCH_SIZE and WRITE_SIZE scaled by a plain copy kernel), or None
     when there is none or it was taken on a different kernel source."""
-    path = os.path.join(PROFILES, f"k_gemm_rows_{workload}_l{layer}_b{batch}.md")
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_l{layer}_b{batch}.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"TRAFFIC_JSON:\s*(\{.*\})", open(path).read())
@@ -222,7 +225,8 @@ def main() -> int:
     log(f"{args.steps} steps in {ms:.3f} ms: {us_layer:.3f} us/layer, {gbs:.1f} GB/s "
         f"({100 * gbs / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f} GB/s)")
 
-    traffic = measured_traffic(args.workload, args.layer, B)
+    kernel = KERNELS[plan["path"]]
+    traffic = measured_traffic(kernel, args.workload, args.layer, B)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -243,7 +247,8 @@ def main() -> int:
             "N": N, "K": K, "q": q, "group": G, "batch": B,
             "weight_copies": copies,
             "launch": "eager" if args.eager else "hip graph replay",
-            "kernel": "k_gemm_splitk" if plan["path"] == 1 else "k_gemm_generic",
+            "kernel": kernel,
+            "rows_per_workgroup": plan["rows_per_wg"],
             "workgroups": plan["workgroups"],
         },
         "us_per_layer": round(us_layer, 4),

@@ -129,7 +129,8 @@ SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const
 
 /* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
 typedef struct {
-    int path;         /* 0: generic kernel (any group), 1: row kernel (group % 128 == 0) */
+    int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel
+                         (batch 1), 2 batch kernel (batch >= 2) */
     int rows_per_wg;  /* output rows per workgroup */
     int workgroups;   /* workgroups of the launch */
     int threads;      /* threads per workgroup */

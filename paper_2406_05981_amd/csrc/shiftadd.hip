@@ -482,6 +482,245 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
 
+// ---------------------------------------------------------------- batch kernel
+//
+// batch >= 2, group % 128 == 0.  A key byte is shared by every batch row, so
+// the tables of four batch rows (a quad) are interleaved: value v of a
+// half-table is a float4 over the quad, and one query reads the four entries
+// with one 16-byte LDS load and adds them into four accumulators.  The address
+// arithmetic of a query is paid once per four batch rows.
+//
+// Work split.  A workgroup owns 16*KW output rows (KW = 1, 2 or 4) and one
+// quad; it walks the input dimension in pieces of 1024 columns, one 128-column
+// block per wave.  Lane (r, p) of a wave handles row r of 16-row group
+// p / (4/KW) and KW of the 4 key words (4 keys each) of that row's block, so a
+// wave covers its block for all 16*KW rows.  Each wave builds the tables of
+// its own block for the quad (lane (c, u) builds chunk c for batch row u of the
+// quad): tables are wave-local and the only workgroup barrier is the final
+// combination of the eight waves' partial sums.
+//
+// LDS layout of a wave's tables (8 KB): float v*128 + h*64 + c*4 + u holds
+// value v of half h (0: columns 8c..8c+3, 1: 8c+4..8c+7) of chunk c for batch
+// row u of the quad.  A query address is one v_perm_b32: byte 1 = (wave << 5)
+// | (v << 1) | h, byte 0 = 16*c.  At one query the 16 lanes of a quarter-wave
+// hold 16 different rows and so (keys rotated by row) 16 different chunks:
+// 16 different 16-byte bank groups.
+
+constexpr int kQuad = 4;                                          // batch rows per table word
+constexpr int kWaveTableFloats = 16 * 2 * kBlockChunks * kQuad;  // 2048 floats = 8 KB
+constexpr int kBatchRows = 64;                                    // most rows per workgroup
+
+struct BatchArgs {
+    const uint16_t* x;  // activations [B][K]
+    const uint8_t* packed;
+    const int8_t* exps;
+    int q, N, K, G, B;
+    float* y;     // [B][N]
+    int n_tiles;  // row tiles of 16*KW rows
+    int n_quads;  // ceil(B / 4)
+};
+
+// One piece for this lane: KW key words of Q planes, their exponents, and the
+// activations of the table chunk the lane builds.
+template <int Q, int KW>
+struct BatchJob {
+    uint32_t w[Q][KW];
+    int e[Q];
+    uint4 xr;
+};
+
+template <int KW>
+__device__ inline void load_words(const uint8_t* p, uint32_t* w) {
+    if constexpr (KW == 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(p);
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else if constexpr (KW == 2) {
+        const uint2 v = *reinterpret_cast<const uint2*>(p);
+        w[0] = v.x; w[1] = v.y;
+    } else {
+        w[0] = *reinterpret_cast<const uint32_t*>(p);
+    }
+}
+
+template <int Q, int KW>
+__device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
+#pragma unroll
+    for (int k = 0; k < KW; ++k) asm volatile("" : "+v"(j.w[i][k]));
+    asm volatile("" : "+v"(j.e[i]));
+}
+
+template <int Q, int KW>
+__device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
+    constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
+    const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, p = lane >> 4;
+    const int dsl = p % DS, rsub = p / DS;
+    // Workgroup -> (row tile, quad).  Workgroups are dealt to the 8 XCDs
+    // round-robin; the quads of one tile land on one XCD and share its L2.
+    const int xcd = blockIdx.x & 7, idx = blockIdx.x >> 3;
+    const int tile = xcd + 8 * (idx / a.n_quads), quad = idx % a.n_quads;
+    if (tile >= a.n_tiles) return;  // whole workgroup: padding of the grid
+    const int row0 = 16 * KW * tile;
+    const int n = imin(row0 + 16 * rsub + r, a.N - 1);
+    const int pieces = (C16 + kRowWaves - 1) / kRowWaves;
+
+    // byte t of offs[k] = 16 * (chunk at key position 4*(KW*dsl + k) + t of row r)
+    uint32_t offs[KW];
+#pragma unroll
+    for (int k = 0; k < KW; ++k) {
+        uint32_t o = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            o |= (uint32_t)(((4 * (KW * dsl + k) + t + r) & 15) << 4) << (8 * t);
+        offs[k] = o;
+    }
+    const uint32_t rgn_lo = (uint32_t)(wave << 5) * 0x01010101u;
+    const uint32_t rgn_hi = (uint32_t)((wave << 5) | 1) * 0x01010101u;
+    const char* lut_bytes = reinterpret_cast<const char*>(lut);
+
+    // this lane's table chunk: chunk r of the wave's block, batch row p of the quad
+    const int bx = imin(kQuad * quad + p, a.B - 1);
+    const int T = n >> 6;
+    const int R = imin(kTileRows, a.N - kTileRows * T);
+    const uint8_t* key_row = a.packed + (int64_t)kTileRows * T * C + 16 * (n & 63) + 4 * KW * dsl;
+    const int8_t* exp_row = a.exps + (int64_t)n * NG;
+
+    auto load_job = [&](int pc, BatchJob<Q, KW>& j) {
+        const int J = imin(kRowWaves * pc + wave, C16 - 1);
+        const int8_t* e = exp_row + (bpg == 1 ? J : J / bpg);
+#pragma unroll
+        for (int i = 0; i < Q; ++i) j.e[i] = e[(int64_t)i * a.N * NG];
+        j.xr = *reinterpret_cast<const uint4*>(a.x + (int64_t)bx * a.K +
+                                               8 * (kBlockChunks * J + r));
+        const uint8_t* kp = key_row + (int64_t)kBlockChunks * J * R;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) load_words<KW>(kp + (int64_t)i * a.N * C, j.w[i]);
+    };
+    auto build = [&](const uint4 xr) {
+        const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
+        float f[8];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
+            f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
+        }
+        float lo[16], hi[16];
+        nibble_sums(f[0], f[1], f[2], f[3], lo);
+        nibble_sums(f[4], f[5], f[6], f[7], hi);
+        float* t = lut + wave * kWaveTableFloats + r * kQuad + p;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            t[v * 128] = lo[v];
+            t[v * 128 + 64] = hi[v];
+        }
+        // the wave's own queries follow; LDS accesses of one wave complete in order
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    float tot[kQuad] = {0.0f, 0.0f, 0.0f, 0.0f};
+    auto query_job = [&](int pc, BatchJob<Q, KW>& j) {
+        // blocks past the end (last piece) repeat the last block: weight 0
+        const float keep = kRowWaves * pc + wave < C16 ? 1.0f : 0.0f;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            __builtin_amdgcn_sched_barrier(0);
+            pin_batch_plane<Q, KW>(j, i);
+            float s[kQuad];
+#pragma unroll
+            for (int k = 0; k < KW; ++k) {
+                // one key word at a time: its 8 loads go out together, then
+                // its adds (32 registers of loads in flight)
+                if (k > 0) __builtin_amdgcn_sched_barrier(0);
+                const uint32_t lo = ((j.w[i][k] << 1) & 0x1e1e1e1eu) | rgn_lo;
+                const uint32_t hi = ((j.w[i][k] >> 3) & 0x1e1e1e1eu) | rgn_hi;
+                float4 L[4], H[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                    L[t] = *reinterpret_cast<const float4*>(
+                        lut_bytes + __builtin_amdgcn_perm(lo, offs[k], sel));
+                    H[t] = *reinterpret_cast<const float4*>(
+                        lut_bytes + __builtin_amdgcn_perm(hi, offs[k], sel));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    if (k == 0 && t == 0) {
+                        s[0] = L[0].x + H[0].x;
+                        s[1] = L[0].y + H[0].y;
+                        s[2] = L[0].z + H[0].z;
+                        s[3] = L[0].w + H[0].w;
+                    } else {
+                        s[0] += L[t].x; s[0] += H[t].x;
+                        s[1] += L[t].y; s[1] += H[t].y;
+                        s[2] += L[t].z; s[2] += H[t].z;
+                        s[3] += L[t].w; s[3] += H[t].w;
+                    }
+                }
+                // the word's adds complete here, so its loads' registers free up
+                asm volatile("" : "+v"(s[0]), "+v"(s[1]), "+v"(s[2]), "+v"(s[3]));
+            }
+#pragma unroll
+            for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
+        }
+    };
+
+    // Two register sets alternate; a piece's keys and activations are
+    // requested before the previous piece's queries, unconditionally (past
+    // the last piece they repeat it), so no register set depends on a branch.
+    BatchJob<Q, KW> ja, jb;
+    load_job(0, ja);
+    for (int pc = 0; pc < pieces; pc += 2) {
+        build(ja.xr);
+        load_job(imin(pc + 1, pieces - 1), jb);
+        query_job(pc, ja);
+        if (pc + 1 >= pieces) break;
+        build(jb.xr);
+        load_job(imin(pc + 2, pieces - 1), ja);
+        query_job(pc + 1, jb);
+    }
+
+    // lanes of one row (fixed order), then the eight waves via LDS
+#pragma unroll
+    for (int u = 0; u < kQuad; ++u) {
+        if constexpr (DS >= 2) tot[u] += __shfl_xor(tot[u], 16);
+        if constexpr (DS == 4) tot[u] += __shfl_xor(tot[u], 32);
+    }
+    if (dsl == 0)
+        *reinterpret_cast<float4*>(red + (wave * kBatchRows + 16 * rsub + r) * kQuad) =
+            make_float4(tot[0], tot[1], tot[2], tot[3]);
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < 16 * KW * kQuad) {
+        const int row = t >> 2, u = t & 3;
+        const int nn = row0 + row, b = kQuad * quad + u;
+        if (nn < a.N && b < a.B) {
+            float s = red[row * kQuad + u];
+#pragma unroll
+            for (int w = 1; w < kRowWaves; ++w) s += red[(w * kBatchRows + row) * kQuad + u];
+            a.y[(int64_t)b * a.N + nn] = s;
+        }
+    }
+}
+
+template <int Q, int KW>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_gemm_batch(BatchArgs a) {
+    __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];  // 64 KB
+    __shared__ float4 red[kRowWaves * kBatchRows];            // 8 KB
+    gemm_batch_body<Q, KW>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+}
+
+template <int Q, int KW>
+__global__ __launch_bounds__(kRowThreads) void k_gemm_batch_wide(BatchArgs a) {
+    __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];
+    __shared__ float4 red[kRowWaves * kBatchRows];
+    gemm_batch_body<Q, KW>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+}
+
 // ---------------------------------------------------------------- host side
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -517,9 +756,43 @@ int rows_rg_per_wg(int q, int N) {
     return rg;
 }
 
+// Batch kernel geometry: rows per workgroup 16*KW.  Every (row tile, quad)
+// pair is one workgroup; KW trades table builds (one per workgroup, quad and
+// piece) against filling the machine.  The estimate counts waves of resident
+// workgroups times the per-piece instructions of one wave (queries of KW key
+// words per plane, about 52 instructions each, plus about 50 for the build).
+int batch_kw(int q, int N, int batch) {
+    const int resident = q <= kRowsResidentQ ? 512 : 256;
+    const int quads = (batch + kQuad - 1) / kQuad;
+    int best_kw = 4;
+    int64_t best = -1;
+    for (int kw = 4; kw >= 1; kw >>= 1) {
+        const int64_t tiles = (N + 16 * kw - 1) / (16 * kw);
+        const int64_t rounds = (tiles * quads + resident - 1) / resident;
+        const int64_t cost = rounds * (52 * kw * q + 50);
+        if (best < 0 || cost < best) {
+            best = cost;
+            best_kw = kw;
+        }
+    }
+    return best_kw;
+}
+
 void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     *p = sa_plan{};
     p->threads = kThreads;
+    if (group % 128 == 0 && batch >= 2) {
+        const int kw = batch_kw(q, N, batch);
+        const int tiles = (N + 16 * kw - 1) / (16 * kw);
+        const int quads = (batch + kQuad - 1) / kQuad;
+        p->path = 2;
+        p->rows_per_wg = 16 * kw;
+        p->workgroups = 8 * quads * ((tiles + 7) / 8);
+        p->pieces = (K / 128 + kRowWaves - 1) / kRowWaves;
+        p->threads = kRowThreads;
+        p->lds_bytes = sizeof(float) * (kRowWaves * kWaveTableFloats + kRowWaves * kBatchRows * kQuad);
+        return;
+    }
     if (group % 128 != 0) {
         p->path = 0;
         p->rows_per_wg = kThreads;
@@ -559,6 +832,27 @@ void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
         case 7: hipLaunchKernelGGL(k_gemm_rows_wide<7>, g, b, 0, s, a); break;
         default: hipLaunchKernelGGL(k_gemm_rows_wide<8>, g, b, 0, s, a); break;
     }
+}
+
+template <int KW>
+void launch_batch_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
+    const dim3 g(workgroups), b(kRowThreads);
+    switch (q) {
+        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW>), g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW>), g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW>), g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW>), g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW>), g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW>), g, b, 0, s, a); break;
+    }
+}
+
+void launch_batch(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t s) {
+    if (kw == 4) launch_batch_kw<4>(q, a, workgroups, s);
+    else if (kw == 2) launch_batch_kw<2>(q, a, workgroups, s);
+    else launch_batch_kw<1>(q, a, workgroups, s);
 }
 
 }  // namespace
@@ -631,6 +925,23 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
         hipLaunchKernelGGL(k_gemm_generic, dim3((N + kThreads - 1) / kThreads, batch),
                            dim3(kThreads), 0, s,
                            x, packed_bits, exps, q, N, K, group, y);
+        return launch_status();
+    }
+    if (plan.path == 2) {
+        BatchArgs a{};
+        a.x = x;
+        a.packed = packed_bits;
+        a.exps = exps;
+        a.q = q;
+        a.N = N;
+        a.K = K;
+        a.G = group;
+        a.B = batch;
+        a.y = y;
+        const int kw = plan.rows_per_wg / 16;
+        a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
+        a.n_quads = (batch + kQuad - 1) / kQuad;
+        launch_batch(q, kw, a, plan.workgroups, s);
         return launch_status();
     }
     RowsArgs a{};

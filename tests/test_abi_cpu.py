@@ -118,10 +118,18 @@ def test_plans():
     assert p["path"] == 1 and p["rows_per_wg"] == 16 and p["workgroups"] == 256
     assert p["pieces"] == 1 and p["lds_bytes"] <= 80 * 1024
     assert sa.sa_plan_gemm(3, 100, 256, 8, 2)["path"] == 0
-    assert sa.sa_plan_gemm(3, 100, 768, 768, 2)["path"] == 1
-    big = sa.sa_plan_gemm(3, 28672, 8192, 128, 8)
-    assert big["pieces"] == 2 and big["rows_per_wg"] % 16 == 0
-    assert big["workgroups"] * big["rows_per_wg"] >= 28672
+    assert sa.sa_plan_gemm(3, 100, 768, 768, 1)["path"] == 1
+    assert sa.sa_plan_gemm(3, 100, 768, 768, 2)["path"] == 2
     assert sa.sa_plan_gemm(3, 8192, 28672, 128, 1)["pieces"] == 7
+    # batch kernel: 1024-column pieces, one workgroup per (row tile, group of 4
+    # batch rows), grid padded to whole rounds of 8 workgroups per XCD
+    big = sa.sa_plan_gemm(3, 28672, 8192, 128, 8)
+    assert big["path"] == 2 and big["pieces"] == 8 and big["rows_per_wg"] == 64
+    assert big["workgroups"] == 8 * 2 * ((28672 // 64 + 7) // 8)
+    assert big["lds_bytes"] <= 80 * 1024
+    # every row-tile height of the batch kernel is reachable
+    heights = {sa.sa_plan_gemm(*c)["rows_per_wg"] for c in
+               [(3, 4100, 384, 384, 13), (3, 4096, 1152, 128, 16), (1, 28672, 1152, 128, 5)]}
+    assert heights == {16, 32, 64}
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm(3, 100, 256, 24, 1)

@@ -136,10 +136,17 @@ def test_build_lut_hand_example():
 # ----------------------------------------------------------------------------- the layer
 
 SMALL = [
-    # split-K table kernel (group % 128 == 0)
-    (1, 1, 128, 128, 1), (3, 65, 256, 128, 1), (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3),
-    (8, 64, 128, 128, 1), (4, 130, 768, 768, 5), (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4),
-    (2, 129, 1152, 384, 7), (3, 4097, 512, 128, 1),
+    # row kernel (group % 128 == 0, batch 1)
+    (1, 1, 128, 128, 1), (3, 65, 256, 128, 1), (8, 64, 128, 128, 1), (3, 4097, 512, 128, 1),
+    (2, 129, 9216, 384, 1),
+    # batch kernel (group % 128 == 0, batch >= 2), 16-row workgroups
+    (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
+    (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),
+    (3, 4100, 384, 384, 13), (8, 40, 384, 128, 6), (6, 300, 2176, 128, 9),
+    # batch kernel, 32-row workgroups
+    (3, 4096, 1152, 128, 16),
+    # batch kernel, 64-row workgroups (last piece and last tile ragged)
+    (1, 28672, 1152, 128, 5), (2, 28000, 256, 256, 8),
     # generic kernel (any group % 8 == 0)
     (3, 100, 256, 8, 2), (1, 1, 8, 8, 1), (2, 257, 200, 40, 3), (3, 64, 1024, 64, 1),
     (4, 70, 96, 24, 1), (2, 33, 136, 136, 2),
