@@ -492,19 +492,27 @@ constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
 //
 // Work split.  A workgroup owns 16*KW output rows (KW = 1, 2 or 4) and one
 // quad; it walks the input dimension in pieces of 1024 columns, one 128-column
-// block per wave.  Lane (r, p) of a wave handles row r of 16-row group
-// p / (4/KW) and KW of the 4 key words (4 keys each) of that row's block, so a
-// wave covers its block for all 16*KW rows.  Each wave builds the tables of
-// its own block for the quad (lane (c, u) builds chunk c for batch row u of the
-// quad): tables are wave-local and the only workgroup barrier is the final
-// combination of the eight waves' partial sums.
+// block per wave.  Each lane handles one row and KW of the 4 key words (4 keys
+// each) of that row's block, so a wave covers its block for all 16*KW rows.
+// Each wave builds the tables of its own block for the quad (lane (c, u)
+// builds chunk c for batch row u of the quad): tables are wave-local and the
+// only workgroup barrier is the final combination of the partial sums.
 //
 // LDS layout of a wave's tables (8 KB): float v*128 + h*64 + c*4 + u holds
 // value v of half h (0: columns 8c..8c+3, 1: 8c+4..8c+7) of chunk c for batch
 // row u of the quad.  A query address is one v_perm_b32: byte 1 = (wave << 5)
-// | (v << 1) | h, byte 0 = 16*c.  At one query the 16 lanes of a quarter-wave
-// hold 16 different rows and so (keys rotated by row) 16 different chunks:
-// 16 different 16-byte bank groups.
+// | (v << 1) | h, byte 0 = 16*c.
+//
+// Bank groups.  A 16-byte LDS read is served 16 lanes at a time: the lanes
+// that agree in lane bit 5 and in the parity of lane bits 2..4 (measured on
+// gfx950 with SQ_LDS_BANK_CONFLICT), and those 16 must touch 16 different
+// 16-byte bank groups (address bits 4..7), i.e. 16 different chunks.  With
+// keys rotated by row, a query at key position pos touches chunk
+// (pos + row) mod 16.  Lane (r, p) (r = lane & 15, p = lane >> 4) therefore
+// takes, for KW = 4: row 16p + r, all words; KW = 2: row 16(p & 1) + r, words
+// 2(p >> 1)..+1 (the two lanes of a half that share r read the same position
+// of different rows); KW = 1: row (r - 4p) mod 16, word p (every lane then
+// queries chunk r + t at step t).  Each 16-lane set covers every chunk once.
 
 constexpr int kQuad = 4;                                          // batch rows per table word
 constexpr int kWaveTableFloats = 16 * 2 * kBlockChunks * kQuad;  // 2048 floats = 8 KB
@@ -555,14 +563,18 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4;
-    const int dsl = p % DS, rsub = p / DS;
+    // key-word slice, 16-row group and row (mod 16) of this lane (see above)
+    const int dsl = KW == 4 ? 0 : KW == 2 ? p >> 1 : p;
+    const int rsub = KW == 4 ? p : KW == 2 ? p & 1 : 0;
+    const int rr = KW == 1 ? (r - 4 * p) & 15 : r;
     // Workgroup -> (row tile, quad).  Workgroups are dealt to the 8 XCDs
     // round-robin; the quads of one tile land on one XCD and share its L2.
     const int xcd = blockIdx.x & 7, idx = blockIdx.x >> 3;
     const int tile = xcd + 8 * (idx / a.n_quads), quad = idx % a.n_quads;
     if (tile >= a.n_tiles) return;  // whole workgroup: padding of the grid
     const int row0 = 16 * KW * tile;
-    const int n = imin(row0 + 16 * rsub + r, a.N - 1);
+    const int row_local = 16 * rsub + rr;
+    const int n = imin(row0 + row_local, a.N - 1);
     const int pieces = (C16 + kRowWaves - 1) / kRowWaves;
 
     // byte t of offs[k] = 16 * (chunk at key position 4*(KW*dsl + k) + t of row r)
@@ -572,7 +584,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
         uint32_t o = 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-            o |= (uint32_t)(((4 * (KW * dsl + k) + t + r) & 15) << 4) << (8 * t);
+            o |= (uint32_t)(((4 * (KW * dsl + k) + t + rr) & 15) << 4) << (8 * t);
         offs[k] = o;
     }
     const uint32_t rgn_lo = (uint32_t)(wave << 5) * 0x01010101u;
@@ -683,24 +695,24 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
         query_job(pc + 1, jb);
     }
 
-    // lanes of one row (fixed order), then the eight waves via LDS
-#pragma unroll
-    for (int u = 0; u < kQuad; ++u) {
-        if constexpr (DS >= 2) tot[u] += __shfl_xor(tot[u], 16);
-        if constexpr (DS == 4) tot[u] += __shfl_xor(tot[u], 32);
-    }
-    if (dsl == 0)
-        *reinterpret_cast<float4*>(red + (wave * kBatchRows + 16 * rsub + r) * kQuad) =
-            make_float4(tot[0], tot[1], tot[2], tot[3]);
+    // Partial sums of (wave, row, word slice) meet in LDS and are added in a
+    // fixed order: waves outer, word slices inner.
+    *reinterpret_cast<float4*>(red + (wave * kBatchRows + row_local * DS + dsl) * kQuad) =
+        make_float4(tot[0], tot[1], tot[2], tot[3]);
     __syncthreads();
     const int t = threadIdx.x;
     if (t < 16 * KW * kQuad) {
         const int row = t >> 2, u = t & 3;
         const int nn = row0 + row, b = kQuad * quad + u;
         if (nn < a.N && b < a.B) {
-            float s = red[row * kQuad + u];
+            float s = red[row * DS * kQuad + u];
 #pragma unroll
-            for (int w = 1; w < kRowWaves; ++w) s += red[(w * kBatchRows + row) * kQuad + u];
+            for (int d = 1; d < DS; ++d) s += red[(row * DS + d) * kQuad + u];
+#pragma unroll
+            for (int w = 1; w < kRowWaves; ++w)
+#pragma unroll
+                for (int d = 0; d < DS; ++d)
+                    s += red[(w * kBatchRows + row * DS + d) * kQuad + u];
             a.y[(int64_t)b * a.N + nn] = s;
         }
     }
