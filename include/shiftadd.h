@@ -54,7 +54,8 @@ extern "C" {
 typedef enum {
     SA_OK = 0,
     SA_ERR_NULL = -1,  /* a required pointer is NULL */
-    SA_ERR_SHAPE = -2, /* N, K or batch out of range, K % 8 != 0, or sizes overflow */
+    SA_ERR_SHAPE = -2, /* N, K or batch out of range, K % 8 != 0, one plane of
+                          packed keys (N*K/8 bytes) >= 2^31, or q*N*K > 2^36 */
     SA_ERR_Q = -3,     /* q outside [1, 8] */
     SA_ERR_GROUP = -4, /* group < 8, group % 8 != 0, or K % group != 0 */
     SA_ERR_ALIGN = -5, /* a pointer that must be 16-byte aligned is not */

@@ -199,19 +199,22 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
 // columns in 64 KB of LDS and build them in a fraction of the time the
 // queries take.
 //
-// LDS layout of a 4096-column piece: 16 regions of 4 KB (two 16-chunk blocks
-// each); value v of half-table `slot` of region rho is the float at byte
-// rho*4096 + v*256 + slot*4.  A query address is one v_perm_b32: byte 1 =
-// (rho << 4) | v (key nibble, region pre-or'ed into the key word), byte 0 =
-// 4*slot.  Slots: chunk u of the region's even block -> (2u, 2u+1) for (lo, hi),
-// odd block -> 32 + (2u+1, 2u) (swapped), odd regions -> slot ^ 32.
+// LDS layout of a 4096-column piece: 256 rows of 64 four-byte slots.  The 32
+// chunks of region rho (blocks 2rho and 2rho+1) keep their low halves in row
+// (rho << 4) | v, slot 16*(block & 1) + u for chunk u of the block, and their
+// high halves in row (v << 4) | rho, slot 32 + 16*(block & 1) + u.  A query
+// address is one v_perm_b32: byte 1 = the key byte masked to the wanted
+// nibble and or-ed with the region (one v_and_or_b32 per 4 keys and half),
+// byte 0 = 4*slot.
 //
 // Work split.  Row r of a 16-row group is handled by lanes r, r+16, r+32,
 // r+48 of all eight waves: part = 4*wave + (lane >> 4) owns block `part` of
 // each piece.  Keys are stored rotated by row (position t of a row's 16 bytes
-// holds chunk (t + row) mod 16), so at each query the 32 lanes of a half-wave
-// touch 32 different slots mod 32 (and the 64 lanes 64 different slots mod
-// 64): no LDS bank conflicts by construction.
+// holds chunk (t + row) mod 16).  A 4-byte LDS read is served one half-wave
+// (32 lanes) at a time, and those lanes must touch 32 different slots mod 32
+// (measured on gfx950 with SQ_LDS_BANK_CONFLICT); the two parts of a
+// half-wave query 2 x 16 different chunks, i.e. 32 different slots: no bank
+// conflicts by construction.
 //
 // Each lane adds the 32 half-entries of its block, shifts the sum by the
 // block's exponent (ldexp) and accumulates in fp32; the 32 lanes of a row are
@@ -248,23 +251,24 @@ struct JobRegs {
 // Exponents are requested before keys (and, for the first job, before the
 // activations): whatever the compiler hoists onto the exponents then waits for
 // them alone, never for the keys behind them.
+// Per-lane offsets are 32-bit (a plane holds fewer than 2^31 bytes) on
+// workgroup-uniform plane bases, so no 64-bit address arithmetic per load.
 template <int Q>
 __device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, int bpg,
                                      JobRegs<Q>& j) {
-    const int8_t* erow = a.exps + (int64_t)n * NG + (bpg == 1 ? J : J / bpg);
+    const uint32_t off = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg));
 #pragma unroll
-    for (int i = 0; i < Q; ++i) j.e[i] = erow[(int64_t)i * a.N * NG];
+    for (int i = 0; i < Q; ++i) j.e[i] = (a.exps + (size_t)i * a.N * NG)[off];
 }
 
 template <int Q>
 __device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, JobRegs<Q>& j) {
     const int T = n >> 6;
     const int R = imin(kTileRows, a.N - kTileRows * T);
-    const uint8_t* base = a.packed + (int64_t)kTileRows * T * C + 16 * (n & 63) +
-                          (int64_t)kBlockChunks * J * R;
+    const uint32_t off = (uint32_t)(kTileRows * T * C + 16 * (n & 63) + kBlockChunks * J * R);
 #pragma unroll
     for (int i = 0; i < Q; ++i)
-        j.w[i] = *reinterpret_cast<const uint4*>(base + (int64_t)i * a.N * C);
+        j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)i * a.N * C + off);
 }
 
 // Empty asm that "may modify" one plane's job registers: their consumers
@@ -280,28 +284,35 @@ __device__ inline void pin_plane(JobRegs<Q>& j, int i) {
 // Planes are consumed in load order, so a plane's queries run while later
 // planes are still arriving.
 template <int Q>
-__device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn, const uint32_t offs[2][4],
-                                const char* lut_bytes) {
+__device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
+                                const uint32_t offs[2][4], const char* lut_bytes) {
     float tot = 0.0f;
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
         __builtin_amdgcn_sched_barrier(0);
         pin_plane<Q>(j, i);
         const uint32_t words[4] = {j.w[i].x, j.w[i].y, j.w[i].z, j.w[i].w};
-        float acc = 0.0f;
+        float acc;
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
-            // key nibbles of 4 bytes, each or'ed with this block's region
-            const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn;
-            const uint32_t hi = ((words[wd] >> 4) & 0x0f0f0f0fu) | rgn;
+            // row byte of each of 4 keys: low nibble | region << 4, and
+            // high nibble (in place) | region
+            const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn_lo;
+            const uint32_t hi = (words[wd] & 0xf0f0f0f0u) | rgn_hi;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                // byte 0: slot offset (offs byte t); byte 1: region|nibble (byte t)
+                // byte 0: slot offset (offs byte t); byte 1: row (byte t)
                 const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
-                acc += *reinterpret_cast<const float*>(
+                const float L = *reinterpret_cast<const float*>(
                     lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
-                acc += *reinterpret_cast<const float*>(
+                const float H = *reinterpret_cast<const float*>(
                     lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
+                if (wd == 0 && t == 0) {
+                    acc = L + H;
+                } else {
+                    acc += L;
+                    acc += H;
+                }
             }
         }
         tot += ldexpf(acc, j.e[i]);
@@ -320,26 +331,20 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     const int nrg = imin(a.rg_per_wg, n_groups - rg0);
     const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
 
-    // Slot offsets of this lane's 16 key positions, low and high nibble (4
-    // positions per register, one per byte), and the region bits of its block,
-    // replicated in every byte's high nibble.  Byte t of offs[nb][wd] is
-    // 4*slot for position 4*wd+t:
-    //   slot = 2*(16*(p&1) + ((pos + r) & 15)) + (nb ^ (p&1)), xor 32 if (p>>1)&1
-    // i.e. 8*((pos + r) & 15) + 4*(nb ^ (p&1)) + 128*((p ^ (p>>1)) & 1).
+    // Slot offsets of this lane's 16 key positions, low and high half (4
+    // positions per register, one per byte): byte t of offs[h][wd] is 4*slot
+    // for position 4*wd+t, slot = 32*h + 16*(p & 1) + ((4*wd + t + r) & 15).
     uint32_t offs[2][4];
-    {
-        const uint32_t hi_bit = (uint32_t)(((p ^ (p >> 1)) & 1) << 7) * 0x01010101u;
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-            // 8*((4*wd + t + r) & 15) for t = 0..3, one per byte
-            const uint32_t base = (uint32_t)(((4 * wd + r) & 15) * 8) * 0x01010101u;
-            const uint32_t steps = (base + 0x18100800u) & 0x78787878u;
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
-                offs[nb][wd] = steps | hi_bit | ((uint32_t)((nb ^ (p & 1)) << 2) * 0x01010101u);
-        }
+    for (int wd = 0; wd < 4; ++wd) {
+        // 4*((4*wd + t + r) & 15) for t = 0..3, one per byte
+        const uint32_t base = (uint32_t)(((4 * wd + r) & 15) * 4) * 0x01010101u;
+        const uint32_t steps = (base + 0x0c080400u) & 0x3c3c3c3cu;
+        offs[0][wd] = steps | (uint32_t)(64 * (p & 1)) * 0x01010101u;
+        offs[1][wd] = offs[0][wd] | 0x80808080u;
     }
-    const uint32_t rgn = (uint32_t)((part >> 1) << 4) * 0x01010101u;
+    const uint32_t rgn_lo = (uint32_t)((part >> 1) << 4) * 0x01010101u;
+    const uint32_t rgn_hi = (uint32_t)(part >> 1) * 0x01010101u;
 
     float acc[kMaxRG];
 #pragma unroll
@@ -356,8 +361,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // `part`), so no table write is ever read by another wave and the only
     // workgroup barrier is the final combination of the waves' row sums.
     const int my_rho = part >> 1;
-    const int slot_lo = ((2 * (16 * (p & 1) + r)) + (p & 1)) ^ (32 * ((p >> 1) & 1));
-    const int slot_hi = slot_lo ^ 1;
+    const int slot_lo = 16 * (p & 1) + r;
+    const int slot_hi = 32 + slot_lo;
     // activations of this lane's table chunk
     auto load_x = [&](int b, int pc) {
         const int c = imin(kPieceChunks * pc + kBlockChunks * part + r, C - 1);
@@ -375,12 +380,13 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         float lo[16], hi[16];
         nibble_sums(f[0], f[1], f[2], f[3], lo);
         nibble_sums(f[4], f[5], f[6], f[7], hi);
+        // low half: row (rho << 4) | v; high half: row (v << 4) | rho
         float* t_lo = lut + my_rho * kRegionFloats + slot_lo;
-        float* t_hi = lut + my_rho * kRegionFloats + slot_hi;
+        float* t_hi = lut + my_rho * 64 + slot_hi;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             t_lo[v * 64] = lo[v];
-            t_hi[v * 64] = hi[v];
+            t_hi[v * kRegionFloats] = hi[v];
         }
         // the wave's own queries follow; LDS accesses of one wave complete in order
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -394,7 +400,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         const int pc = (job / nrg) % pieces;
         const int b = job / (nrg * pieces);
         const bool valid = kPieceBlocks * pc + part < C16;
-        const float v = job_sum<Q>(regs, rgn, offs, lut_bytes);
+        const float v = job_sum<Q>(regs, rgn_lo, rgn_hi, offs, lut_bytes);
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
             if (gg == g && valid) acc[gg] += v;
@@ -740,8 +746,10 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int check_dims(int q, int N, int K) {
     if (q < 1 || q > SA_MAX_Q) return SA_ERR_Q;
     if (N < 1 || K < 8 || (K & 7)) return SA_ERR_SHAPE;
-    // every element count that the kernels index must fit comfortably
+    // every element count that the kernels index must fit comfortably; one
+    // plane of packed keys stays below 2^31 bytes (32-bit per-lane offsets)
     if ((int64_t)q * N * K > (int64_t)1 << 36) return SA_ERR_SHAPE;
+    if ((int64_t)N * (K / 8) >= (int64_t)1 << 31) return SA_ERR_SHAPE;
     return SA_OK;
 }
 

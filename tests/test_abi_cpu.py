@@ -89,6 +89,9 @@ def test_gemm_validation_codes():
     assert _gemm(K=0) == sa.SA_ERR_SHAPE
     assert _gemm(B=0) == sa.SA_ERR_SHAPE
     assert _gemm(B=sa.SA_MAX_BATCH + 1) == sa.SA_ERR_SHAPE
+    # one plane of packed keys must stay below 2^31 bytes
+    assert sa.sa_packed_bytes(1, 1 << 17, 1 << 17) == 0
+    assert sa.sa_packed_bytes(1, (1 << 17) - 1, 1 << 17) == ((1 << 17) - 1) * (1 << 14)
     assert _gemm(G=0) == sa.SA_ERR_GROUP
     assert _gemm(G=12) == sa.SA_ERR_GROUP
     assert _gemm(G=96) == sa.SA_ERR_GROUP  # 256 % 96 != 0

@@ -138,7 +138,9 @@ def test_build_lut_hand_example():
 SMALL = [
     # row kernel (group % 128 == 0, batch 1)
     (1, 1, 128, 128, 1), (3, 65, 256, 128, 1), (8, 64, 128, 128, 1), (3, 4097, 512, 128, 1),
-    (2, 129, 9216, 384, 1),
+    (2, 129, 9216, 384, 1), (3, 17, 4224, 128, 1),
+    # row kernel whose exponents exceed the LDS staging budget (read directly)
+    (8, 300, 65536, 128, 1),
     # batch kernel (group % 128 == 0, batch >= 2), 16-row workgroups
     (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
     (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),
@@ -159,6 +161,21 @@ def test_gemm_small(q, N, K, G, B):
     c = workloads.random_case(q, N, K, G, B, seed=1, exp_range=(-10, -2), outlier_fraction=0.01)
     y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], G)
     check(gemm(c), y_ref, a_ref, c["name"])
+
+
+@pytest.mark.parametrize("B", [1, 5])
+def test_exps_at_odd_address(B):
+    """Exponents may start at any byte address: the staged copy then falls back
+    to byte loads."""
+    say(f"exps at odd address B={B}")
+    c = workloads.random_case(3, 200, 1024, 128, B, seed=2, exp_range=(-10, -2))
+    y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], 128)
+    flat = c["exps"].reshape(-1)
+    buf = torch.zeros(flat.size + 1, dtype=torch.int8, device="cuda")
+    buf[1:] = dev(flat)
+    e = buf[1:]
+    assert e.data_ptr() % 2 == 1
+    check(gemm(c, exps=e), y_ref, a_ref, "odd exps address")
 
 
 def test_gemm_hand_example():
