@@ -500,9 +500,11 @@ constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
 // quad; it walks the input dimension in pieces of 1024 columns, one 128-column
 // block per wave.  Each lane handles one row and KW of the 4 key words (4 keys
 // each) of that row's block, so a wave covers its block for all 16*KW rows.
-// Each wave builds the tables of its own block for the quad (lane (c, u)
-// builds chunk c for batch row u of the quad): tables are wave-local and the
-// only workgroup barrier is the final combination of the partial sums.
+// Each wave builds the tables of its own block for the quad, one (chunk, batch
+// row) per lane: lane l builds chunk (l & 7) + 8*(l >> 5) for batch row
+// (l >> 3) & 3, so the 32 lanes of a half-wave write 32 different 4-byte
+// banks.  Tables are wave-local and the only workgroup barrier is the final
+// combination of the partial sums.
 //
 // LDS layout of a wave's tables (8 KB): float v*128 + h*64 + c*4 + u holds
 // value v of half h (0: columns 8c..8c+3, 1: 8c+4..8c+7) of chunk c for batch
@@ -597,8 +599,9 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     const uint32_t rgn_hi = (uint32_t)((wave << 5) | 1) * 0x01010101u;
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
 
-    // this lane's table chunk: chunk r of the wave's block, batch row p of the quad
-    const int bx = imin(kQuad * quad + p, a.B - 1);
+    // this lane's table chunk and batch row of the quad (see above)
+    const int bc = (lane & 7) + 8 * (lane >> 5), bu = (lane >> 3) & 3;
+    const int bx = imin(kQuad * quad + bu, a.B - 1);
     const int T = n >> 6;
     const int R = imin(kTileRows, a.N - kTileRows * T);
     const uint8_t* key_row = a.packed + (int64_t)kTileRows * T * C + 16 * (n & 63) + 4 * KW * dsl;
@@ -610,7 +613,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
         for (int i = 0; i < Q; ++i) j.e[i] = e[(int64_t)i * a.N * NG];
         j.xr = *reinterpret_cast<const uint4*>(a.x + (int64_t)bx * a.K +
-                                               8 * (kBlockChunks * J + r));
+                                               8 * (kBlockChunks * J + bc));
         const uint8_t* kp = key_row + (int64_t)kBlockChunks * J * R;
 #pragma unroll
         for (int i = 0; i < Q; ++i) load_words<KW>(kp + (int64_t)i * a.N * C, j.w[i]);
@@ -626,7 +629,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
         float lo[16], hi[16];
         nibble_sums(f[0], f[1], f[2], f[3], lo);
         nibble_sums(f[4], f[5], f[6], f[7], hi);
-        float* t = lut + wave * kWaveTableFloats + r * kQuad + p;
+        float* t = lut + wave * kWaveTableFloats + bc * kQuad + bu;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             t[v * 128] = lo[v];
