@@ -132,7 +132,8 @@ SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const
 typedef struct {
     int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel
                          (batch 1), 2 batch kernel (batch >= 2) */
-    int rows_per_wg;  /* output rows per workgroup */
+    int rows_per_wg;  /* output rows per workgroup (the largest share when the
+                         row kernel spreads row groups unevenly) */
     int workgroups;   /* workgroups of the launch */
     int threads;      /* threads per workgroup */
     int pieces;       /* input-dimension pieces whose tables a workgroup builds in turn */

@@ -188,8 +188,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
 
 // ---------------------------------------------------------------- row kernel
 //
-// group % 128 == 0.  Each workgroup owns 16*rg_per_wg output rows over the
-// whole input dimension, so no partial sums ever leave a workgroup.
+// group % 128 == 0.  Each workgroup owns a contiguous range of 16-row groups
+// over the whole input dimension, so no partial sums ever leave a workgroup.
+// The row groups are spread evenly over the workgroups (counts differ by at
+// most one), so no compute unit carries more rows than the average rounded up.
 //
 // Tables.  The 256-entry table of chunk c (Sec. 4.1) is stored factored into
 // its two 16-entry halves: lo_c[v] = sum_{j<4} (bit j of v ? +x : -x)[8c+j] and
@@ -216,6 +218,11 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
 // half-wave query 2 x 16 different chunks, i.e. 32 different slots: no bank
 // conflicts by construction.
 //
+// Jobs.  A job is (batch row, piece, row group), row group fastest; a lane's
+// share of a job is one 16-byte key load per plane and one exponent per plane.
+// Loads run D - 1 jobs ahead of the queries, in a ring of D register sets, so
+// every wave keeps the next jobs' keys in flight while it works.
+//
 // Each lane adds the 32 half-entries of its block, shifts the sum by the
 // block's exponent (ldexp) and accumulates in fp32; the 32 lanes of a row are
 // then combined in a fixed order (two xor-shuffles, then the eight waves via
@@ -237,20 +244,37 @@ struct RowsArgs {
     const int8_t* exps;
     int q, N, K, G, B;
     float* y;           // [B][N]
-    int rg_per_wg;      // row groups per workgroup (<= kMaxRG)
+    int groups;         // 16-row groups of N, spread over the grid
 };
 
-// Keys and exponents of one (row group, piece) job for this lane: Q planes of
-// one block.
+// Keys and exponents of one job for this lane (Q planes of one block), and the
+// activations of the lane's table chunk when the job starts a piece.
 template <int Q>
 struct JobRegs {
     uint4 w[Q];
     int e[Q];  // exponent (sign-extending byte load)
+    uint4 xr;
 };
 
-// Exponents are requested before keys (and, for the first job, before the
-// activations): whatever the compiler hoists onto the exponents then waits for
-// them alone, never for the keys behind them.
+// Position of a job inside the workgroup's sequence: row group g (fastest),
+// piece pc, batch row b.
+struct JobPos {
+    int g, pc, b;
+};
+
+__device__ inline void next_pos(JobPos& j, int nrg, int pieces) {
+    if (++j.g == nrg) {
+        j.g = 0;
+        if (++j.pc == pieces) {
+            j.pc = 0;
+            ++j.b;
+        }
+    }
+}
+
+// Exponents are requested before keys (and before the activations): whatever
+// the compiler hoists onto the exponents then waits for them alone, never for
+// the keys behind them.
 // Per-lane offsets are 32-bit (a plane holds fewer than 2^31 bytes) on
 // workgroup-uniform plane bases, so no 64-bit address arithmetic per load.
 template <int Q>
@@ -320,16 +344,19 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
     return tot;
 }
 
-template <int Q>
+template <int Q, int D>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
-    const int rg0 = blockIdx.x * a.rg_per_wg;
-    const int n_groups = (a.N + kGroupRows - 1) / kGroupRows;
-    const int nrg = imin(a.rg_per_wg, n_groups - rg0);
+    // row groups of this workgroup: the first `extra` workgroups take one more
+    const int wgs = (int)gridDim.x, wg = (int)blockIdx.x;
+    const int base = a.groups / wgs, extra = a.groups - base * wgs;
+    const int nrg = base + (wg < extra ? 1 : 0);
+    const int rg0 = wg * base + imin(wg, extra);
     const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
+    const int jobs = a.B * pieces * nrg;
 
     // Slot offsets of this lane's 16 key positions, low and high half (4
     // positions per register, one per byte): byte t of offs[h][wd] is 4*slot
@@ -338,8 +365,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 #pragma unroll
     for (int wd = 0; wd < 4; ++wd) {
         // 4*((4*wd + t + r) & 15) for t = 0..3, one per byte
-        const uint32_t base = (uint32_t)(((4 * wd + r) & 15) * 4) * 0x01010101u;
-        const uint32_t steps = (base + 0x0c080400u) & 0x3c3c3c3cu;
+        const uint32_t base4 = (uint32_t)(((4 * wd + r) & 15) * 4) * 0x01010101u;
+        const uint32_t steps = (base4 + 0x0c080400u) & 0x3c3c3c3cu;
         offs[0][wd] = steps | (uint32_t)(64 * (p & 1)) * 0x01010101u;
         offs[1][wd] = offs[0][wd] | 0x80808080u;
     }
@@ -351,11 +378,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     for (int g = 0; g < kMaxRG; ++g) acc[g] = 0.0f;
 
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
-    const int jobs = a.B * pieces * nrg;  // (batch row, piece, row group), row group fastest
-    auto job_row = [&](int job) { return imin(kGroupRows * (rg0 + job % nrg) + r, a.N - 1); };
-    auto job_block = [&](int job) {
-        return imin(kPieceBlocks * ((job / nrg) % pieces) + part, C16 - 1);
-    };
+    auto row_of = [&](const JobPos& j) { return imin(kGroupRows * (rg0 + j.g) + r, a.N - 1); };
+    auto block_of = [&](const JobPos& j) { return imin(kPieceBlocks * j.pc + part, C16 - 1); };
     // Tables are wave-local: the 64 lanes of a wave build the 64 chunks of the
     // four blocks that wave queries (lane (r, p) builds chunk r of block
     // `part`), so no table write is ever read by another wave and the only
@@ -364,9 +388,9 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     const int slot_lo = 16 * (p & 1) + r;
     const int slot_hi = 32 + slot_lo;
     // activations of this lane's table chunk
-    auto load_x = [&](int b, int pc) {
-        const int c = imin(kPieceChunks * pc + kBlockChunks * part + r, C - 1);
-        return *reinterpret_cast<const uint4*>(a.x + (int64_t)b * a.K + 8 * c);
+    auto load_x = [&](const JobPos& j) {
+        const int c = imin(kPieceChunks * j.pc + kBlockChunks * part + r, C - 1);
+        return *reinterpret_cast<const uint4*>(a.x + (int64_t)j.b * a.K + 8 * c);
     };
     // tables of this wave's four blocks of one piece for one batch row
     auto build = [&](const uint4 xr) {
@@ -393,18 +417,23 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
+    // Requests of one job: exponents, then the activations when the job starts
+    // a piece (its tables are built just before its queries), then keys.
+    auto load_job = [&](const JobPos& j, JobRegs<Q>& regs) {
+        const int n = row_of(j), J = block_of(j);
+        load_job_exps<Q>(a, n, J, NG, bpg, regs);
+        if (j.g == 0) regs.xr = load_x(j);
+        load_job_keys<Q>(a, n, J, C, regs);
+    };
     // queries of one job, accumulation into its row group, and -- when the job
     // completes batch row b -- the combination of the 32 lanes of every row
-    auto run_job = [&](int job, JobRegs<Q>& regs) {
-        const int g = job % nrg;
-        const int pc = (job / nrg) % pieces;
-        const int b = job / (nrg * pieces);
-        const bool valid = kPieceBlocks * pc + part < C16;
+    auto run_job = [&](const JobPos& j, JobRegs<Q>& regs) {
+        const bool valid = kPieceBlocks * j.pc + part < C16;
         const float v = job_sum<Q>(regs, rgn_lo, rgn_hi, offs, lut_bytes);
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
-            if (gg == g && valid) acc[gg] += v;
-        if (pc == pieces - 1 && g == nrg - 1) {
+            if (gg == j.g && valid) acc[gg] += v;
+        if (j.pc == pieces - 1 && j.g == nrg - 1) {
 #pragma unroll
             for (int gg = 0; gg < kMaxRG; ++gg) {
                 if (gg < nrg) {
@@ -422,52 +451,63 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                     float s = red[0][t];
 #pragma unroll
                     for (int w = 1; w < kRowWaves; ++w) s += red[w][t];
-                    a.y[(int64_t)b * a.N + n] = s;
+                    a.y[(int64_t)j.b * a.N + n] = s;
                 }
             }
             __syncthreads();  // red is rewritten by the next batch row
         }
     };
-    auto load_job_n = [&](int job, JobRegs<Q>& regs) {
-        const int n = job_row(job), J = job_block(job);
-        load_job_exps<Q>(a, n, J, NG, bpg, regs);
-        load_job_keys<Q>(a, n, J, C, regs);
-    };
-    // Job 0: exponents, activations, then keys, so the first table build waits
-    // for the activations only while the keys stay in flight.
-    auto prologue = [&](JobRegs<Q>& j0) {
-        load_job_exps<Q>(a, job_row(0), job_block(0), NG, bpg, j0);
-        const uint4 xr = load_x(0, 0);
-        load_job_keys<Q>(a, job_row(0), job_block(0), C, j0);
-        __builtin_amdgcn_sched_barrier(0);
-        build(xr);
-        __builtin_amdgcn_sched_barrier(0);
-    };
 
+    JobPos run{0, 0, 0};
     if (jobs == 1) {
+        // one job: exponents, activations, keys; the table build waits for the
+        // activations only while the keys stay in flight
         JobRegs<Q> j0;
-        prologue(j0);
-        run_job(0, j0);
+        load_job(run, j0);
+        __builtin_amdgcn_sched_barrier(0);
+        build(j0.xr);
+        __builtin_amdgcn_sched_barrier(0);
+        run_job(run, j0);
         return;
     }
-    // Several jobs: two register sets alternate (no copies of pending loads);
-    // each job's keys (and, when it starts a piece, its activations) are
-    // requested before the previous job's queries.  The key requests are
-    // unconditional -- past the last job they repeat it -- so no register set
-    // depends on a branch.
-    JobRegs<Q> ja, jb;
-    prologue(ja);
-    for (int job = 0; job < jobs; job += 2) {
-        if (job > 0 && job % nrg == 0) build(load_x(job / (nrg * pieces), (job / nrg) % pieces));
-        load_job_n(imin(job + 1, jobs - 1), jb);
-        run_job(job, ja);
-        if (job + 1 >= jobs) break;
-        if ((job + 1) % nrg == 0)
-            build(load_x((job + 1) / (nrg * pieces), ((job + 1) / nrg) % pieces));
-        load_job_n(imin(job + 2, jobs - 1), ja);
-        run_job(job + 1, jb);
+    // Several jobs: a ring of D register sets.  Job k + D - 1 is requested
+    // before job k's table build and queries; past the last job the requests
+    // repeat it, so every request is unconditional and no register set depends
+    // on a branch.
+    JobRegs<Q> ring[D];
+    JobPos ld{0, 0, 0};
+    int loaded = 0;  // last job requested
+    load_job(ld, ring[0]);
+#pragma unroll
+    for (int k = 1; k < D - 1; ++k) {
+        if (loaded + 1 < jobs) {
+            next_pos(ld, nrg, pieces);
+            ++loaded;
+        }
+        load_job(ld, ring[k]);
+    }
+    for (int job = 0; job < jobs; job += D) {
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+            if (job + k >= jobs) break;
+            if (loaded + 1 < jobs) {
+                next_pos(ld, nrg, pieces);
+                ++loaded;
+            }
+            load_job(ld, ring[(k + D - 1) % D]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (run.g == 0) build(ring[k].xr);
+            __builtin_amdgcn_sched_barrier(0);
+            run_job(run, ring[k]);
+            next_pos(run, nrg, pieces);
+        }
     }
 }
+
+// Ring depth: two job register sets (a third measured slower on gfx950: the
+// extra registers cost more than the deeper prefetch gains).
+template <int Q>
+constexpr int rows_ring() { return 2; }
 
 // Up to 4 planes: two 8-wave workgroups per CU (4 waves per SIMD, <= 128
 // VGPRs).  More planes need more registers: one workgroup per CU.
@@ -476,14 +516,14 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4))
 void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q>(a, lut, red);
+    gemm_rows_body<Q, rows_ring<Q>()>(a, lut, red);
 }
 
 template <int Q>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q>(a, lut, red);
+    gemm_rows_body<Q, rows_ring<Q>()>(a, lut, red);
 }
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
@@ -767,16 +807,16 @@ int validate_gemm(const void* x, const void* packed, const void* exps, int q, in
     return SA_OK;
 }
 
-int rows_rg_per_wg(int q, int N) {
-    // As many workgroups as are resident at once (two per CU up to 3 planes,
-    // one beyond), every workgroup taking a contiguous range of 16-row groups
-    // and reusing its tables across them.
+// Row kernel grid: as many workgroups as are resident at once (two per CU up
+// to kRowsResidentQ planes, one beyond), or fewer when there are fewer row
+// groups; more only when a workgroup would otherwise hold more than kMaxRG
+// row groups.  The kernel spreads the row groups evenly over the grid.
+int rows_workgroups(int q, int N) {
     const int resident = q <= kRowsResidentQ ? 512 : 256;
     const int groups = (N + kGroupRows - 1) / kGroupRows;
-    int rg = (groups + resident - 1) / resident;
-    if (rg < 1) rg = 1;
-    if (rg > kMaxRG) rg = kMaxRG;
-    return rg;
+    int w = groups < resident ? groups : resident;
+    if ((groups + w - 1) / w > kMaxRG) w = (groups + kMaxRG - 1) / kMaxRG;
+    return w;
 }
 
 // Batch kernel geometry: rows per workgroup 16*KW.  Every (row tile, quad)
@@ -824,11 +864,11 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
         p->lds_bytes = sizeof(float) * (kBlockChunks * 256 + SA_MAX_Q * kThreads);
         return;
     }
-    const int rg = rows_rg_per_wg(q, N);
     const int groups = (N + kGroupRows - 1) / kGroupRows;
+    const int wgs = rows_workgroups(q, N);
     p->path = 1;
-    p->rows_per_wg = kGroupRows * rg;
-    p->workgroups = (groups + rg - 1) / rg;
+    p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);  // the largest share
+    p->workgroups = wgs;
     p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
     p->threads = kRowThreads;
     p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
@@ -977,7 +1017,7 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.G = group;
     a.B = batch;
     a.y = y;
-    a.rg_per_wg = plan.rows_per_wg / kGroupRows;
+    a.groups = (N + kGroupRows - 1) / kGroupRows;
     launch_rows(q, a, plan.workgroups, s);
     return launch_status();
 }
