@@ -220,8 +220,6 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
 //
 // Jobs.  A job is (batch row, piece, row group), row group fastest; a lane's
 // share of a job is one 16-byte key load per plane and one exponent per plane.
-// Loads run D - 1 jobs ahead of the queries, in a ring of D register sets, so
-// every wave keeps the next jobs' keys in flight while it works.
 //
 // Each lane adds the 32 half-entries of its block, shifts the sum by the
 // block's exponent (ldexp) and accumulates in fp32; the 32 lanes of a row are
@@ -252,7 +250,7 @@ struct RowsArgs {
 template <int Q>
 struct JobRegs {
     uint4 w[Q];
-    int e[Q];  // exponent (sign-extending byte load)
+    uint32_t e[Q];  // exponent byte, zero-extended; sign-extended where it is used
     uint4 xr;
 };
 
@@ -272,9 +270,8 @@ __device__ inline void next_pos(JobPos& j, int nrg, int pieces) {
     }
 }
 
-// Exponents are requested before keys (and before the activations): whatever
-// the compiler hoists onto the exponents then waits for them alone, never for
-// the keys behind them.
+// Exponents are requested before keys: whatever the compiler hoists onto the
+// exponents then waits for them alone, never for the keys behind them.
 // Per-lane offsets are 32-bit (a plane holds fewer than 2^31 bytes) on
 // workgroup-uniform plane bases, so no 64-bit address arithmetic per load.
 template <int Q>
@@ -282,7 +279,8 @@ __device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, in
                                      JobRegs<Q>& j) {
     const uint32_t off = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg));
 #pragma unroll
-    for (int i = 0; i < Q; ++i) j.e[i] = (a.exps + (size_t)i * a.N * NG)[off];
+    for (int i = 0; i < Q; ++i)
+        j.e[i] = reinterpret_cast<const uint8_t*>(a.exps + (size_t)i * a.N * NG)[off];
 }
 
 template <int Q>
@@ -339,12 +337,12 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
                 }
             }
         }
-        tot += ldexpf(acc, j.e[i]);
+        tot += ldexpf(acc, (int)(int8_t)j.e[i]);
     }
     return tot;
 }
 
-template <int Q, int D>
+template <int Q, int U>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
@@ -417,12 +415,15 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
-    // Requests of one job: exponents, then the activations when the job starts
-    // a piece (its tables are built just before its queries), then keys.
+    // Requests of one job: the activations when the job starts a piece (its
+    // tables are built just before its queries, so they are asked for first),
+    // then exponents, then keys.
     auto load_job = [&](const JobPos& j, JobRegs<Q>& regs) {
         const int n = row_of(j), J = block_of(j);
-        load_job_exps<Q>(a, n, J, NG, bpg, regs);
         if (j.g == 0) regs.xr = load_x(j);
+        __builtin_amdgcn_sched_barrier(0);
+        load_job_exps<Q>(a, n, J, NG, bpg, regs);
+        __builtin_amdgcn_sched_barrier(0);
         load_job_keys<Q>(a, n, J, C, regs);
     };
     // queries of one job, accumulation into its row group, and -- when the job
@@ -458,56 +459,63 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         }
     };
 
-    JobPos run{0, 0, 0};
+    // One job at a time: its requests (activations first, then exponents,
+    // then keys), the table build when the job starts a piece, the queries.
+    // Latency is hidden by the other waves resident on the SIMD rather than by
+    // prefetching into a second register set: a loop-carried set of pending
+    // loads makes the compiler copy registers at the loop back-edge, which
+    // waits for every outstanding load and costs more than it hides.
+    JobPos j{0, 0, 0};
     if (jobs == 1) {
-        // one job: exponents, activations, keys; the table build waits for the
-        // activations only while the keys stay in flight
-        JobRegs<Q> j0;
-        load_job(run, j0);
+        // A single job (a layer of at most 4096 columns and 16 rows per
+        // workgroup): every request goes out at once, with no ordering
+        // constraint, and the table build waits for the activations only.
+        JobRegs<Q> regs;
+        regs.xr = load_x(j);
+        load_job_exps<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
+        load_job_keys<Q>(a, row_of(j), block_of(j), C, regs);
         __builtin_amdgcn_sched_barrier(0);
-        build(j0.xr);
+        build(regs.xr);
         __builtin_amdgcn_sched_barrier(0);
-        run_job(run, j0);
+        run_job(j, regs);
         return;
     }
-    // Several jobs: a ring of D register sets.  Job k + D - 1 is requested
-    // before job k's table build and queries; past the last job the requests
-    // repeat it, so every request is unconditional and no register set depends
-    // on a branch.
-    JobRegs<Q> ring[D];
-    JobPos ld{0, 0, 0};
-    int loaded = 0;  // last job requested
-    load_job(ld, ring[0]);
+    // Several jobs: U jobs per iteration.  All their requests go out at the
+    // top of the iteration (past the last job they repeat it), then the jobs
+    // are worked through in order, each waiting only for its own loads.  No
+    // load is pending across the loop back-edge, so the compiler keeps every
+    // register set in place, and a wave has U jobs of keys in flight per
+    // round trip to memory.
+    for (int job = 0; job < jobs; job += U) {
+        JobRegs<Q> regs[U];
+        JobPos pos[U];
+        pos[0] = j;
 #pragma unroll
-    for (int k = 1; k < D - 1; ++k) {
-        if (loaded + 1 < jobs) {
-            next_pos(ld, nrg, pieces);
-            ++loaded;
+        for (int u = 1; u < U; ++u) {
+            pos[u] = pos[u - 1];
+            if (job + u < jobs) next_pos(pos[u], nrg, pieces);
         }
-        load_job(ld, ring[k]);
-    }
-    for (int job = 0; job < jobs; job += D) {
 #pragma unroll
-        for (int k = 0; k < D; ++k) {
-            if (job + k >= jobs) break;
-            if (loaded + 1 < jobs) {
-                next_pos(ld, nrg, pieces);
-                ++loaded;
+        for (int u = 0; u < U; ++u) load_job(pos[u], regs[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (job + u < jobs) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (pos[u].g == 0) build(regs[u].xr);
+                __builtin_amdgcn_sched_barrier(0);
+                run_job(pos[u], regs[u]);
             }
-            load_job(ld, ring[(k + D - 1) % D]);
-            __builtin_amdgcn_sched_barrier(0);
-            if (run.g == 0) build(ring[k].xr);
-            __builtin_amdgcn_sched_barrier(0);
-            run_job(run, ring[k]);
-            next_pos(run, nrg, pieces);
         }
+        j = pos[U - 1];
+        next_pos(j, nrg, pieces);
     }
 }
 
-// Ring depth: two job register sets (a third measured slower on gfx950: the
-// extra registers cost more than the deeper prefetch gains).
+// Jobs per loop iteration.  One: requesting several jobs' keys at once
+// measured slower on gfx950 (the layer is bound by LDS and VALU issue, not by
+// memory latency, and the extra registers only add pressure).
 template <int Q>
-constexpr int rows_ring() { return 2; }
+constexpr int rows_jobs_per_iter() { return 1; }
 
 // Up to 4 planes: two 8-wave workgroups per CU (4 waves per SIMD, <= 128
 // VGPRs).  More planes need more registers: one workgroup per CU.
@@ -516,14 +524,14 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4))
 void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_ring<Q>()>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>()>(a, lut, red);
 }
 
 template <int Q>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_ring<Q>()>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>()>(a, lut, red);
 }
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
