@@ -145,10 +145,12 @@ SMALL = [
     (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
     (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),
     (3, 4100, 384, 384, 13), (8, 40, 384, 128, 6), (6, 300, 2176, 128, 9),
-    # batch kernel, 32-row workgroups
-    (3, 4096, 1152, 128, 16),
+    # batch kernel, 32-row workgroups over two pieces
+    (3, 4096, 2304, 128, 16),
     # batch kernel, 64-row workgroups (last piece and last tile ragged)
     (1, 28672, 1152, 128, 5), (2, 28000, 256, 256, 8),
+    # batch kernel, 128-row workgroups, eight quads
+    (1, 28600, 256, 128, 32),
     # generic kernel (any group % 8 == 0)
     (3, 100, 256, 8, 2), (1, 1, 8, 8, 1), (2, 257, 200, 40, 3), (3, 64, 1024, 64, 1),
     (4, 70, 96, 24, 1), (2, 33, 136, 136, 2),
@@ -161,6 +163,23 @@ def test_gemm_small(q, N, K, G, B):
     c = workloads.random_case(q, N, K, G, B, seed=1, exp_range=(-10, -2), outlier_fraction=0.01)
     y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], G)
     check(gemm(c), y_ref, a_ref, c["name"])
+
+
+@pytest.mark.parametrize("B", [2, 5, 8])
+def test_batch_large_activations(B):
+    """Activations near the top of the fp16 range in some blocks of some batch
+    rows, next to fp16 subnormals and in a ragged last piece: table values reach
+    about 2.4e5 and must stay exact to fp32 rounding."""
+    say(f"batch large activations B={B}")
+    c = workloads.random_case(3, 300, 2304, 128, B, seed=21)
+    x = c["x"].astype(np.float32)
+    x[0, 130:140] = 30000.0          # block 1, first batch row
+    x[B - 1, 1000] = -60000.0        # block 7, last batch row
+    x[B - 1, 1001:1004] = 3e-7       # fp16 subnormals next to it
+    x[B // 2, 2200:2300] = 9000.0    # last (partial) piece, just above 8192
+    c["x"] = x.astype(np.float16)
+    y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], 128)
+    check(gemm(c), y_ref, a_ref, "large activations")
 
 
 @pytest.mark.parametrize("B", [1, 5])
