@@ -90,7 +90,7 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
         t0 = time.perf_counter()
         oracle.shiftadd_gemm(d["x"], d["signs"], d["exps"], d["G"], nthreads=threads, rows=sel)
         times.append(time.perf_counter() - t0)
-        if len(times) >= 3 and time.perf_counter() > deadline or len(times) >= 50:
+        if len(times) >= 3 and time.perf_counter() > deadline or len(times) >= 100000:
             break
     t = sorted(times)[len(times) // 2]
     us_layer = t * 1e6 * N / rows
@@ -98,6 +98,45 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
               f"median of {len(times)} runs, fp64 oracle, OpenMP")
     return {"value": bytes_step / us_layer / 1e3, "unit": "GB/s", "cores": used, "kind": "oracle",
             "sample": sample, "us_per_layer": us_layer}
+
+
+def time_read_floor(sa, nbytes: int, rotate_mb: float, steps: int, stream) -> dict:
+    """A plain read of the same number of bytes (sa_read_probe), over its own
+    rotating buffers (>= rotate_mb in total) and replayed from a HIP graph like
+    the layer: what the layer's byte count costs with no work on it."""
+    import torch
+
+    nb = (nbytes + 15) // 16 * 16
+    copies = max(1, math.ceil(rotate_mb * 1e6 / nb))
+    pool = torch.empty(copies * nb, dtype=torch.uint8, device="cuda")
+    pool.fill_(0x5A)
+    out = torch.empty(256, dtype=torch.float32, device="cuda")
+    bufs = [pool[i * nb:(i + 1) * nb] for i in range(copies)]
+    with torch.cuda.stream(stream):
+        for b in bufs:
+            sa.sa_read_probe(b, nb, out)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for b in bufs:
+            sa.sa_read_probe(b, nb, out)
+    with torch.cuda.stream(stream):
+        g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, steps // copies)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for _ in range(reps):
+            g.replay()
+        end.record(stream)
+    torch.cuda.synchronize()
+    us = start.elapsed_time(end) * 1e3 / (reps * copies)
+    del pool, bufs
+    return {"us_per_layer": round(us, 4), "bytes": nb, "achieved": round(nb / us / 1e3, 2),
+            "unit": "GB/s", "what": "sa_read_probe: a plain read of the layer's algorithmic "
+            "byte count, same rotation and graph replay"}
 
 
 def main() -> int:
@@ -113,9 +152,12 @@ def main() -> int:
     ap.add_argument("--eager", action="store_true",
                     help="launch every step from Python instead of replaying a graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=4.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="wall time of the CPU oracle sample (repeated runs, median taken)")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain device copy of this many MB (counter calibration)")
+    ap.add_argument("--no-read-floor", action="store_true",
+                    help="skip timing a plain read of the layer's bytes (sa_read_probe)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -225,6 +267,11 @@ def main() -> int:
     log(f"{args.steps} steps in {ms:.3f} ms: {us_layer:.3f} us/layer, {gbs:.1f} GB/s "
         f"({100 * gbs / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f} GB/s)")
 
+    read_floor = None
+    if not args.no_read_floor:
+        read_floor = time_read_floor(sa, bytes_step, args.rotate_mb, args.steps, stream)
+        log(f"read floor: {read_floor}")
+
     kernel = KERNELS[plan["path"]]
     traffic = measured_traffic(kernel, args.workload, args.layer, B)
     out = {
@@ -264,6 +311,9 @@ def main() -> int:
             "traffic": traffic,
         },
     }
+    if read_floor is not None:
+        out["read_floor"] = read_floor
+        out["frac_of_read_floor"] = round(read_floor["us_per_layer"] / us_layer, 4)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(d0, bytes_step, args.cpu_seconds)

@@ -142,6 +142,17 @@ typedef struct {
 
 SA_API int sa_plan_gemm(int q, int N, int K, int group, int batch, sa_plan *plan);
 
+/* Measurement aid, not part of the layer (no operation of the paper): reads
+ * every byte of `buf` once -- each thread three 16-byte words, grid-strided, so
+ * every wave request is 1 KiB of contiguous memory -- and writes at most one
+ * float per wave into out[] (values unspecified).  Its time is that
+ * of a plain read of `bytes` bytes, the practical floor a layer that streams as
+ * many bytes is compared against.
+ *   buf    (device) 16-byte aligned; bytes a multiple of 16, 16 <= bytes <= 2^40.
+ *   out    (device) float [256], overwritten.
+ * Asynchronous on `stream`. */
+SA_API int sa_read_probe(const void *buf, size_t bytes, float *out, void *stream);
+
 /* Human-readable text for a status code (static storage). */
 SA_API const char *sa_status_string(int status);
 

@@ -45,6 +45,7 @@ def _bind(lib):
         "sa_build_lut": ([P, I, I, P, P], I),
         "sa_shiftadd_gemm": ([P, P, P, I, I, I, I, I, P, P], I),
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
+        "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
         "sa_version": ([], ctypes.c_char_p),
     }
@@ -155,6 +156,17 @@ def sa_shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Ten
         _dev(exps, "exps", torch.int8, q * N * (K // group)),
         q, N, K, group, batch,
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm")
+
+
+def sa_read_probe(buf: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None) -> None:
+    """Plain read of ``nbytes`` bytes of ``buf`` (a measurement aid, see the header)."""
+    if not isinstance(buf, torch.Tensor) or not buf.is_cuda:
+        raise ValueError("buf must be a GPU tensor")
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the buffer")
+    _check(lib.sa_read_probe(buf.data_ptr(), nbytes,
+                             _dev(out, "out", torch.float32, 256), _stream(stream)),
+           "sa_read_probe")
 
 
 # ------------------------------------------------------------------ conveniences

@@ -136,3 +136,13 @@ def test_plans():
     assert heights == {16, 32, 64}
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm(3, 100, 256, 24, 1)
+
+
+def test_read_probe_validation_codes():
+    f = sa.lib.sa_read_probe
+    assert f(None, 1024, A, None) == sa.SA_ERR_NULL
+    assert f(A, 1024, None, None) == sa.SA_ERR_NULL
+    assert f(A, 0, A, None) == sa.SA_ERR_SHAPE
+    assert f(A, 1000, A, None) == sa.SA_ERR_SHAPE  # not a multiple of 16
+    assert f(A, (1 << 40) + 16, A, None) == sa.SA_ERR_SHAPE
+    assert f(A + 8, 1024, A, None) == sa.SA_ERR_ALIGN
