@@ -860,19 +860,20 @@ int rows_workgroups(int q, int N) {
 }
 
 // Batch kernel geometry: rows per workgroup 16*KW.  Every (row tile, quad)
-// pair is one workgroup; KW trades table builds (one per workgroup, quad and
-// piece) against filling the machine.  The estimate counts waves of resident
-// workgroups times the per-piece instructions of one wave (queries of KW key
-// words per plane, about 52 instructions each, plus about 50 for the build).
+// pair is one workgroup, and the kernel is bound by LDS work, which the
+// workgroups resident on a CU share: per workgroup and piece the queries cost
+// about 16.5*rows*q LDS cycles (two 16-byte reads per key and quad) and the
+// table build about 1144 (eight waves of 32 four-byte writes, which cost about
+// four times as much per byte as the reads); a CU runs ceil(workgroups / 256)
+// workgroups.  The KW with the least LDS work on the busiest CU wins.
 int batch_kw(int q, int N, int batch) {
-    const int resident = q <= kRowsResidentQ ? 512 : 256;
-    const int quads = (batch + kQuad - 1) / kQuad;
-    int best_kw = 4;
-    int64_t best = -1;
-    for (int kw = 4; kw >= 1; kw >>= 1) {
-        const int64_t tiles = (N + 16 * kw - 1) / (16 * kw);
-        const int64_t rounds = (tiles * quads + resident - 1) / resident;
-        const int64_t cost = rounds * (52 * kw * q + 50);
+    const int64_t quads = (batch + kQuad - 1) / kQuad;
+    int best_kw = 1;
+    double best = -1;
+    for (int kw = 1; kw <= 4; kw <<= 1) {
+        const int64_t rows = 16 * kw;
+        const int64_t wgs = (N + rows - 1) / rows * quads;
+        const double cost = (double)((wgs + 255) / 256) * (16.5 * (double)rows * q + 1144.0);
         if (best < 0 || cost < best) {
             best = cost;
             best_kw = kw;
