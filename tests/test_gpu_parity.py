@@ -145,11 +145,11 @@ SMALL = [
     (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
     (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),
     (3, 4100, 384, 384, 13), (8, 40, 384, 128, 6), (6, 300, 2176, 128, 9),
-    # batch kernel, 32-row workgroups over two pieces
+    # batch kernel, 64-row workgroups over three pieces
     (3, 4096, 2304, 128, 16),
     # batch kernel, 64-row workgroups (last piece and last tile ragged)
     (1, 28672, 1152, 128, 5), (2, 28000, 256, 256, 8),
-    # batch kernel, 128-row workgroups, eight quads
+    # batch kernel, 64-row workgroups, eight quads
     (1, 28600, 256, 128, 32),
     # generic kernel (any group % 8 == 0)
     (3, 100, 256, 8, 2), (1, 1, 8, 8, 1), (2, 257, 200, 40, 3), (3, 64, 1024, 64, 1),
