@@ -139,11 +139,144 @@ def time_read_floor(sa, nbytes: int, rotate_mb: float, steps: int, stream) -> di
             "byte count, same rotation and graph replay"}
 
 
+QUANT_METRIC = "µs per layer of the offline reparameterization (BCQ + power-of-two scales)"
+FP64_PEAK_TFLOPS = 78.6  # MI355X, published fp64 vector peak
+
+
+def quant_algorithmic(q: int, N: int, K: int, G: int, T: int):
+    """(bytes, fp64 ops) one quantization of an N x K layer must spend at
+    minimum: read the fp32 weights, write q int8 sign planes and the int8
+    exponents; per weight 2q fp64 ops for the greedy residuals and their sums,
+    and per cycle q adds for B^T w plus 2^q distances and 2^q comparisons for
+    the nearest code value."""
+    nbytes = 4 * N * K + q * N * K + q * N * (K // G)
+    ops = N * K * (2 * q + T * (q + 2 * (1 << q)))
+    return nbytes, ops
+
+
+def cpu_baseline_quant(w, q: int, G: int, T: int, seconds: float) -> dict:
+    """The CPU oracle (oracle/bcq.py, numpy, fp64) on a bounded sample of rows
+    of the same layer."""
+    import numpy as np
+    from oracle import bcq
+
+    N, K = w.shape
+    t0 = time.perf_counter()
+    bcq.quantize(w[:1], q, G, T)
+    per_row = time.perf_counter() - t0
+    rows = int(min(N, max(1, seconds / 3 / max(per_row, 1e-9))))
+    times = []
+    deadline = time.perf_counter() + seconds
+    while True:
+        t0 = time.perf_counter()
+        bcq.quantize(w[:rows], q, G, T)
+        times.append(time.perf_counter() - t0)
+        if len(times) >= 3 and time.perf_counter() > deadline or len(times) >= 1000:
+            break
+    t = sorted(times)[len(times) // 2]
+    us_layer = t * 1e6 * N / rows
+    return {"value": round(us_layer, 1), "unit": "us/layer", "cores": 1, "kind": "oracle",
+            "sample": f"first {rows} of {N} rows, median of {len(times)} runs, fp64 numpy "
+                      "oracle (one thread), scaled to the whole layer"}
+
+
+def bench_quantize(args) -> int:
+    """Times sa_quantize_bcq on one layer shape (default: the LLaMA-2-7B
+    attention projection, 4096 x 4096, q = 3, G = 128, T = 2 cycles)."""
+    import numpy as np
+    import torch
+
+    import workloads
+    import paper_2406_05981_amd.shiftadd as sa
+
+    q, G, T = args.q, args.group, args.cycles
+    N, K = args.shape
+    steps = args.steps if args.steps is not None else 200
+    warmup = args.warmup if args.warmup is not None else 20
+    in_bytes = 4 * N * K
+    copies = max(1, math.ceil(args.rotate_mb * 1e6 / in_bytes))
+    log(f"quantize N={N} K={K} q={q} G={G} T={T}: {copies} weight copies")
+    t0 = time.perf_counter()
+    w0 = workloads.fp_weights(N, K, seed=1)
+    ws = [torch.from_numpy(w0).cuda()]
+    for c in range(1, copies):
+        ws.append(torch.from_numpy(workloads.fp_weights(N, K, seed=1 + c)).cuda())
+    signs = [torch.empty((q, N, K), dtype=torch.int8, device="cuda") for _ in range(copies)]
+    exps = [torch.empty((q, N, K // G), dtype=torch.int8, device="cuda") for _ in range(copies)]
+    torch.cuda.synchronize()
+    log(f"weights generated in {time.perf_counter() - t0:.1f} s")
+    stream = torch.cuda.Stream()
+
+    def step(i: int) -> None:
+        c = i % copies
+        sa.sa_quantize_bcq(ws[c], N, K, q, G, T, signs[c], exps[c])
+
+    with torch.cuda.stream(stream):
+        for i in range(max(warmup, copies)):
+            step(i)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for i in range(steps):
+            step(i)
+        end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    us = ms * 1e3 / steps
+    nbytes, ops = quant_algorithmic(q, N, K, G, T)
+    gbs = nbytes / us / 1e3
+    tflops = ops / us / 1e6
+    t_hbm = nbytes / (HBM_PEAK_GBS * 1e3)
+    t_alu = ops / (FP64_PEAK_TFLOPS * 1e6)
+    bound = "hbm" if t_hbm >= t_alu else "alu"
+    log(f"{steps} launches in {ms:.3f} ms: {us:.2f} us/layer; {gbs:.1f} GB/s, "
+        f"{tflops:.2f} fp64 TFLOP/s; floors hbm {t_hbm:.2f} us, fp64 {t_alu:.2f} us")
+    out = {
+        "metric": QUANT_METRIC,
+        "value": round(us, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": us / 1e3,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded fp32 weights: N(0, 0.02^2) scaled per row by a log-normal "
+                "factor, 0.1% entries x10)",
+        "config": {"workload": f"bcq_{N}x{K}", "N": N, "K": K, "q": q, "group": G, "cycles": T,
+                   "weight_copies": copies, "launch": "eager", "kernel": f"k_quantize_bcq<{q}>"},
+        "weights_per_s": round(N * K / us * 1e6, 1),
+        "roofline": {
+            "bound": bound,
+            "achieved": round(gbs if bound == "hbm" else tflops, 3),
+            "peak": HBM_PEAK_GBS if bound == "hbm" else FP64_PEAK_TFLOPS,
+            "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+            "frac": round((t_hbm if bound == "hbm" else t_alu) / us, 4),
+            "traffic": None,
+            "algorithmic_bytes": nbytes,
+            "algorithmic_fp64_ops": ops,
+            "floor_us": {"hbm": round(t_hbm, 3), "fp64": round(t_alu, 3)},
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline_quant(w0, q, G, T, args.cpu_seconds)
+        log(f"cpu baseline: {out['cpu_baseline']}")
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=4000)
-    ap.add_argument("--warmup", type=int, default=400)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 4000; "
+                    "200 with --quantize)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 400; "
+                    "20 with --quantize)")
     ap.add_argument("--workload", default="llama2_7b_attn")
     ap.add_argument("--layer", type=int, default=0)
     ap.add_argument("--batch", type=int, default=None)
@@ -158,6 +291,13 @@ def main() -> int:
                     help="only run a plain device copy of this many MB (counter calibration)")
     ap.add_argument("--no-read-floor", action="store_true",
                     help="skip timing a plain read of the layer's bytes (sa_read_probe)")
+    ap.add_argument("--quantize", action="store_true",
+                    help="time the offline reparameterization (sa_quantize_bcq) instead")
+    ap.add_argument("--shape", type=int, nargs=2, default=(4096, 4096), metavar=("N", "K"),
+                    help="--quantize: weight shape")
+    ap.add_argument("--q", type=int, default=3, help="--quantize: binary planes")
+    ap.add_argument("--group", type=int, default=128, help="--quantize: group size")
+    ap.add_argument("--cycles", type=int, default=2, help="--quantize: alternating cycles")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -176,6 +316,13 @@ def main() -> int:
         log("bench.py needs a GPU")
         return 1
     torch.cuda.set_device(0)
+
+    if args.quantize:
+        return bench_quantize(args)
+    if args.steps is None:
+        args.steps = 4000
+    if args.warmup is None:
+        args.warmup = 400
 
     if args.copy_calibration_mb > 0:
         n = int(args.copy_calibration_mb * 1e6) // 4

@@ -65,6 +65,7 @@ typedef enum {
 /* Largest accepted values. */
 #define SA_MAX_Q 8
 #define SA_MAX_BATCH 256
+#define SA_MAX_CYCLES 64
 
 /* Bytes of the packed planes of a q x N x K layer: q*N*K/8 (1 bit per weight
  * per plane, no padding).  Returns 0 for invalid sizes. */
@@ -127,6 +128,35 @@ SA_API int sa_build_lut(const uint16_t *x, int K, int batch, float *lut, void *s
  * call may be captured in a HIP graph. */
 SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
                             int q, int N, int K, int group, int batch, float *y, void *stream);
+
+/* The offline reparameterization that produces the layer's planes and
+ * exponents from full-precision weights: alternating multi-bit binary-coding
+ * quantization (Sec. 3, Alg. 1: greedy initialisation on residuals, Eq. 1, then
+ * `cycles` rounds of a least-squares refit of the scales and a refit of the
+ * codes) with every scale rounded to a power of two (Sec. 4.1, Eq. 2, one
+ * term).  Each segment of `group` consecutive columns of one row is quantized
+ * on its own, in fp64:
+ *   greedy   r = w; for i < q: b_i = sign(r) (sign(0) = +1),
+ *            alpha_i = sum|r| / group, r -= alpha_i b_i;
+ *   cycle    LS: alpha = (B^T B)^-1 B^T w (Gaussian elimination with partial
+ *            pivoting; a column whose pivot is <= 1e-9 * group depends on the
+ *            earlier ones and gets alpha = 0);  PoT: alpha -> sign * 2^P with
+ *            P = round(log2|alpha|) in the log domain (|alpha| = m 2^E,
+ *            m in [1, 2): P = E + [m >= sqrt 2]), clamped to [-128, 127], and
+ *            alpha = 0 -> P = -128;  BS: each element takes the codes whose
+ *            value sum_i +-alpha_i is nearest to it (ties: the smaller code
+ *            number, b_i = +1 when bit i is set).
+ * With cycles = 0 the greedy scales are rounded to powers of two.  The result
+ * is the layer's format: W_q[n][k] = sum_i 2^exps[i][n][k/group] *
+ * signs[i][n][k], the sign of each scale folded into its plane.
+ *   w      (device) fp32 [N][K], row-major, 4-byte aligned.
+ *   q in [1, 8]; group % 8 == 0, K % group == 0; cycles in [0, SA_MAX_CYCLES].
+ *   signs  (device) int8 [q][N][K], +-1, fully overwritten (the input of
+ *          sa_pack_weights).
+ *   exps   (device) int8 [q][N][K/group], fully overwritten.
+ * Asynchronous on `stream`; deterministic. */
+SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int cycles,
+                           int8_t *signs, int8_t *exps, void *stream);
 
 /* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
 typedef struct {

@@ -7,8 +7,8 @@ library has not been built (``python -m paper_2406_05981_amd.build``).
 """
 __all__ = [
     "sa_packed_bytes", "sa_packed_offset", "sa_pack_weights", "sa_unpack_weights",
-    "sa_build_lut", "sa_shiftadd_gemm", "sa_plan_gemm", "sa_read_probe", "sa_status_string",
-    "sa_version",
+    "sa_build_lut", "sa_shiftadd_gemm", "sa_plan_gemm", "sa_quantize_bcq", "sa_read_probe",
+    "sa_status_string", "sa_version", "quantize_bcq",
     "pack_weights", "shiftadd_gemm", "SaError",
 ]
 

@@ -11,7 +11,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "shiftadd.hip")]
+SOURCES = [os.path.join(HERE, "csrc", "shiftadd.hip"), os.path.join(HERE, "csrc", "bcq.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libshiftadd.so")
 ARCH = "gfx950"

@@ -46,6 +46,7 @@ def _bind(lib):
         "sa_shiftadd_gemm": ([P, P, P, I, I, I, I, I, P, P], I),
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
+        "sa_quantize_bcq": ([P, I, I, I, I, I, P, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
         "sa_version": ([], ctypes.c_char_p),
     }
@@ -62,6 +63,7 @@ SA_OK, SA_ERR_NULL, SA_ERR_SHAPE, SA_ERR_Q, SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_H
     0, -1, -2, -3, -4, -5, -6)
 SA_MAX_Q = 8
 SA_MAX_BATCH = 256
+SA_MAX_CYCLES = 64
 
 
 class SaError(RuntimeError):
@@ -158,6 +160,17 @@ def sa_shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Ten
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm")
 
 
+def sa_quantize_bcq(w: torch.Tensor, N: int, K: int, q: int, group: int, cycles: int,
+                    signs: torch.Tensor, exps: torch.Tensor, stream=None) -> None:
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_quantize_bcq")
+    _check(lib.sa_quantize_bcq(
+        _dev(w, "w", torch.float32, N * K), N, K, q, group, cycles,
+        _dev(signs, "signs", torch.int8, q * N * K),
+        _dev(exps, "exps", torch.int8, q * N * (K // group)), _stream(stream)),
+        "sa_quantize_bcq")
+
+
 def sa_read_probe(buf: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None) -> None:
     """Plain read of ``nbytes`` bytes of ``buf`` (a measurement aid, see the header)."""
     if not isinstance(buf, torch.Tensor) or not buf.is_cuda:
@@ -170,6 +183,16 @@ def sa_read_probe(buf: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None
 
 
 # ------------------------------------------------------------------ conveniences
+
+def quantize_bcq(w: torch.Tensor, q: int, group: int, cycles: int, stream=None):
+    """``(signs int8 [q][N][K], exps int8 [q][N][K/group])`` of fp32 weights
+    ``[N][K]`` (new device tensors), in the layer's format."""
+    N, K = w.shape
+    signs = torch.empty((q, N, K), dtype=torch.int8, device=w.device)
+    exps = torch.empty((q, N, K // group), dtype=torch.int8, device=w.device)
+    sa_quantize_bcq(w, N, K, q, group, cycles, signs, exps, stream)
+    return signs, exps
+
 
 def pack_weights(signs: torch.Tensor, stream=None) -> torch.Tensor:
     """Packed planes of ``int8 [q][N][K]`` signs (a new uint8 device tensor)."""

@@ -147,3 +147,24 @@ def test_read_probe_validation_codes():
     assert f(A, 1000, A, None) == sa.SA_ERR_SHAPE  # not a multiple of 16
     assert f(A, (1 << 40) + 16, A, None) == sa.SA_ERR_SHAPE
     assert f(A + 8, 1024, A, None) == sa.SA_ERR_ALIGN
+
+
+def test_quantize_validation_codes():
+    f = sa.lib.sa_quantize_bcq
+
+    def call(w=A, N=16, K=256, q=3, G=128, T=2, s=A, e=A):
+        return f(w, N, K, q, G, T, s, e, None)
+
+    assert call(w=None) == sa.SA_ERR_NULL
+    assert call(s=None) == sa.SA_ERR_NULL
+    assert call(e=None) == sa.SA_ERR_NULL
+    assert call(q=0) == sa.SA_ERR_Q
+    assert call(q=9) == sa.SA_ERR_Q
+    assert call(N=0) == sa.SA_ERR_SHAPE
+    assert call(K=12) == sa.SA_ERR_SHAPE
+    assert call(G=0) == sa.SA_ERR_GROUP
+    assert call(G=12) == sa.SA_ERR_GROUP
+    assert call(G=96) == sa.SA_ERR_GROUP   # 256 % 96 != 0
+    assert call(T=-1) == sa.SA_ERR_SHAPE
+    assert call(T=sa.SA_MAX_CYCLES + 1) == sa.SA_ERR_SHAPE
+    assert call(w=A + 2) == sa.SA_ERR_ALIGN

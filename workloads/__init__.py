@@ -17,6 +17,12 @@ What is drawn, per layer of shape N x K with q binary planes and group size G
   outliers, round(0.01 K) channels (the same for every batch row, drawn without
   replacement) are multiplied by 20 before the cast to fp16.
 
+For the offline reparameterization (full-precision weights -> planes and
+exponents), ``fp_weights`` draws fp32 ``[N][K]`` stand-ins for pretrained
+projection weights: N(0, scale^2) scaled per row by a log-normal factor
+(exp(N(0, 0.25^2))), with a fraction of entries multiplied by
+``outlier_scale`` (the heavy tail of LLM weights).
+
 Draw order per layer is fixed: signs, exps, x, outlier channels, from
 ``numpy.random.default_rng(SeedSequence([seed, config_id, layer_id]))``.
 
@@ -42,6 +48,7 @@ __all__ = [
     "random_case",
     "mixed_bits",
     "sha256",
+    "fp_weights",
 ]
 
 
@@ -212,3 +219,20 @@ def random_case(q: int, N: int, K: int, G: int, B: int, seed: int = 0,
     return dict(signs=signs, exps=exps, x=x16, outlier_channels=idx, q=q, N=N, K=K, G=G, B=B,
                 name=f"case(q={q},N={N},K={K},G={G},B={B},seed={seed})", seed=seed, copy=0)
 
+
+
+def fp_weights(N: int, K: int, seed: int = 0, scale: float = 0.02,
+               outlier_fraction: float = 1e-3, outlier_scale: float = 10.0) -> np.ndarray:
+    """Seeded fp32 weights [N][K] for the offline reparameterization.
+
+    Draw order: per-row factors, the Gaussian body, then the outlier positions
+    (uniform over the N*K entries, with replacement; a repeated position is
+    scaled once)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 200, N, K]))
+    rows = np.exp(0.25 * rng.standard_normal((N, 1)))
+    w = rng.standard_normal((N, K)) * (scale * rows)
+    n_out = int(round(outlier_fraction * N * K))
+    if n_out > 0:
+        idx = np.unique(rng.integers(0, N * K, size=n_out))
+        w.reshape(-1)[idx] *= outlier_scale
+    return w.astype(np.float32)
