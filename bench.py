@@ -154,6 +154,27 @@ def quant_algorithmic(q: int, N: int, K: int, G: int, T: int):
     return nbytes, ops
 
 
+QUANT_SRC = os.path.join(ROOT, "paper_2406_05981_amd", "csrc", "bcq.hip")
+
+
+def measured_traffic_quant(kernel: str, N: int, K: int, q: int, G: int, T: int):
+    """HBM bytes per quantizer launch from the committed rocprofv3 counter summary
+    of this shape, or None when there is none or it was taken on other source."""
+    path = os.path.join(PROFILES, f"{kernel}_bcq_{N}x{K}_q{q}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"TRAFFIC_JSON:\s*(\{.*\})", open(path).read())
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    with open(QUANT_SRC, "rb") as f:
+        src = hashlib.sha256(f.read()).hexdigest()[:16]
+    if (rec.get("source_sha256_16") != src or rec.get("group") != G or rec.get("cycles") != T
+            or rec.get("q") != q):
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def cpu_baseline_quant(w, q: int, G: int, T: int, seconds: float) -> dict:
     """The CPU oracle (oracle/bcq.py, numpy, fp64) on a bounded sample of rows
     of the same layer."""
@@ -231,6 +252,8 @@ def bench_quantize(args) -> int:
     t_hbm = nbytes / (HBM_PEAK_GBS * 1e3)
     t_alu = ops / (FP64_PEAK_TFLOPS * 1e6)
     bound = "hbm" if t_hbm >= t_alu else "alu"
+    # groups of at most 256 go to the register kernel, larger ones to one wave each
+    kernel = "k_quantize_seg" if G <= 256 else "k_quantize_bcq"
     log(f"{steps} launches in {ms:.3f} ms: {us:.2f} us/layer; {gbs:.1f} GB/s, "
         f"{tflops:.2f} fp64 TFLOP/s; floors hbm {t_hbm:.2f} us, fp64 {t_alu:.2f} us")
     out = {
@@ -248,7 +271,7 @@ def bench_quantize(args) -> int:
         "data": "synthetic (seeded fp32 weights: N(0, 0.02^2) scaled per row by a log-normal "
                 "factor, 0.1% entries x10)",
         "config": {"workload": f"bcq_{N}x{K}", "N": N, "K": K, "q": q, "group": G, "cycles": T,
-                   "weight_copies": copies, "launch": "eager", "kernel": f"k_quantize_bcq<{q}>"},
+                   "weight_copies": copies, "launch": "eager", "kernel": kernel},
         "weights_per_s": round(N * K / us * 1e6, 1),
         "roofline": {
             "bound": bound,
@@ -256,7 +279,7 @@ def bench_quantize(args) -> int:
             "peak": HBM_PEAK_GBS if bound == "hbm" else FP64_PEAK_TFLOPS,
             "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
             "frac": round((t_hbm if bound == "hbm" else t_alu) / us, 4),
-            "traffic": None,
+            "traffic": measured_traffic_quant(kernel, N, K, q, G, T),
             "algorithmic_bytes": nbytes,
             "algorithmic_fp64_ops": ops,
             "floor_us": {"hbm": round(t_hbm, 3), "fp64": round(t_alu, 3)},

@@ -149,12 +149,14 @@ SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const
  * With cycles = 0 the greedy scales are rounded to powers of two.  The result
  * is the layer's format: W_q[n][k] = sum_i 2^exps[i][n][k/group] *
  * signs[i][n][k], the sign of each scale folded into its plane.
- *   w      (device) fp32 [N][K], row-major, 4-byte aligned.
+ *   w      (device) fp32 [N][K], row-major, finite, 16-byte aligned.
  *   q in [1, 8]; group % 8 == 0, K % group == 0; cycles in [0, SA_MAX_CYCLES].
- *   signs  (device) int8 [q][N][K], +-1, fully overwritten (the input of
- *          sa_pack_weights).
+ *   signs  (device) int8 [q][N][K], +-1, 8-byte aligned, fully overwritten
+ *          (the input of sa_pack_weights).
  *   exps   (device) int8 [q][N][K/group], fully overwritten.
- * Asynchronous on `stream`; deterministic. */
+ * Errors: SA_ERR_NULL, SA_ERR_Q, SA_ERR_SHAPE (sizes as for the layer, or
+ * cycles out of range), SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_HIP.
+ * Asynchronous on `stream`; deterministic; allocates nothing. */
 SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int cycles,
                            int8_t *signs, int8_t *exps, void *stream);
 

@@ -168,3 +168,6 @@ def test_quantize_validation_codes():
     assert call(T=-1) == sa.SA_ERR_SHAPE
     assert call(T=sa.SA_MAX_CYCLES + 1) == sa.SA_ERR_SHAPE
     assert call(w=A + 2) == sa.SA_ERR_ALIGN
+    assert call(w=A + 8) == sa.SA_ERR_ALIGN   # 16-byte loads
+    assert call(s=A + 4) == sa.SA_ERR_ALIGN   # 8-byte stores
+    assert call(e=A + 1, w=None) == sa.SA_ERR_NULL  # exps may be unaligned

@@ -109,7 +109,10 @@ SHAPES = [
     (6, 9, 200, 40, 3, "q=6, G=40 (ragged lanes)"),
     (7, 12, 192, 192, 1, "q=7, G=K=192"),
     (8, 33, 512, 64, 2, "q=8, 256-entry code table"),
-    (3, 5, 4096, 4096, 2, "q=3, G=K=4096 (64 elements per lane)"),
+    (3, 5, 4096, 4096, 2, "q=3, G=K=4096 (wave per segment, 64 elements per lane)"),
+    (2, 20, 1056, 264, 2, "q=2, G=264 (wave per segment, ragged lanes)"),
+    (4, 6, 2048, 512, 3, "q=4, G=512 (wave per segment)"),
+    (6, 9, 1024, 512, 2, "q=6, G=512 (wave per segment, table in LDS)"),
 ]
 
 
@@ -119,10 +122,12 @@ def test_quantize_parity(q, N, K, G, T, label):
     check_parity(w, q, G, T, label)
 
 
-def test_quantize_edge_values():
+@pytest.mark.parametrize("G", [64, 512])
+def test_quantize_edge_values(G):
     """Zero segments, constant segments, exactly representable ties, fp32
-    extremes (power-of-two exponents clamped to [-128, 127]) and subnormals."""
-    q, G, T = 3, 64, 2
+    extremes (power-of-two exponents clamped to [-128, 127]) and subnormals,
+    through both kernels (16 lanes per segment, and one wave per segment)."""
+    q, T = 3, 2
     rows = []
     rows.append(np.zeros(256))
     rows.append(np.full(256, 0.375))
@@ -133,9 +138,9 @@ def test_quantize_edge_values():
                                 np.linspace(-1, 1, 128)]))
     rng = np.random.default_rng(5)
     rows.append(rng.choice([-0.25, 0.25, 0.75, -0.75], size=256))   # 2-plane PoT values
-    w = np.stack(rows).astype(np.float32)
+    w = np.tile(np.stack(rows), (1, 2)).astype(np.float32)
     for T_ in (0, T):
-        s, e = check_parity(w, q, G, T_, f"edge values T={T_}")
+        s, e = check_parity(w, q, G, T_, f"edge values G={G} T={T_}")
     # the fp32 extremes clamp at the top of the exponent range
     assert e[:, 3].max() == 127
     # zero segments: no scale, all exponents at the bottom of the range
