@@ -18,6 +18,11 @@ computes, with the passage it follows:
   ``W_q = sum_i 2^{e_i} b_i`` (Sec. 3 BCQ with the power-of-two factors of
   Eq. 2, one factor per plane, row and group of G columns), and the sum of the
   magnitudes of its terms (the tolerance reference).
+* :func:`shiftadd_gemm_colwise` -- the layer with column-wise scaling factors
+  ("Ours (Acc.)", Sec. 4.2): one power-of-two factor per plane and weight
+  column, ``W_q[n][k] = sum_i 2^{e_i[k]} b_i[n][k]``, so that
+  ``y = sum_i sum_k b_i[n][k] 2^{e_i[k]} x[k]`` (the factor shifts the
+  activation it meets).
 """
 from __future__ import annotations
 
@@ -68,6 +73,9 @@ def _load():
     lib.oracle_shiftadd_gemm_rows.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64,
                                               P, P, ctypes.c_int]
     lib.oracle_shiftadd_gemm_rows.restype = None
+    lib.oracle_shiftadd_gemm_colwise.argtypes = [P, P, P, I64, I64, I64, I64, P, I64,
+                                                 P, P, ctypes.c_int]
+    lib.oracle_shiftadd_gemm_colwise.restype = None
     _lib = lib
     return lib
 
@@ -151,4 +159,35 @@ def shiftadd_gemm(x: np.ndarray, signs: np.ndarray, exps: np.ndarray, G: int,
         a = np.empty((B, r.size), dtype=np.float64)
         lib.oracle_shiftadd_gemm_rows(_ptr(x64), _ptr(signs), _ptr(exps), q, N, K, G, B,
                                       _ptr(r), r.size, _ptr(y), _ptr(a), int(nthreads))
+    return y, a
+
+
+def shiftadd_gemm_colwise(x: np.ndarray, signs: np.ndarray, col_exps: np.ndarray,
+                          nthreads: int = 0, rows: Optional[Sequence[int]] = None
+                          ) -> Tuple[np.ndarray, np.ndarray]:
+    """``(y, absterm)``, fp64 ``[B][N]`` (or ``[B][len(rows)]``), of the layer with
+    column-wise factors: ``y[b][n] = sum_i sum_k s_i[n][k] ldexp(x[b][k], e[i][k])``
+    and ``absterm[b][n] = sum_i sum_k 2^e[i][k] |x[b][k]|``."""
+    x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    col_exps = np.ascontiguousarray(col_exps, dtype=np.int8)
+    q, N, K = signs.shape
+    B = x64.shape[0]
+    if col_exps.shape != (q, K):
+        raise ValueError(f"col_exps shape {col_exps.shape} != {(q, K)}")
+    if x64.shape != (B, K):
+        raise ValueError(f"x shape {x64.shape} != {(B, K)}")
+    lib = _load()
+    if rows is None:
+        r, R, rp = None, N, None
+    else:
+        r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        if r.size and (r.min() < 0 or r.max() >= N):
+            raise ValueError("row index out of range")
+        R, rp = r.size, _ptr(r)
+    y = np.empty((B, R), dtype=np.float64)
+    a = np.empty((B, R), dtype=np.float64)
+    lib.oracle_shiftadd_gemm_colwise(_ptr(x64), _ptr(signs), _ptr(col_exps), q, N, K, B,
+                                     rp, R if r is not None else 0, _ptr(y), _ptr(a),
+                                     int(nthreads))
     return y, a

@@ -164,3 +164,49 @@ void oracle_shiftadd_gemm_rows(const double *x, const int8_t *signs, const int8_
             if (absterm) absterm[b * nrows + t] = a;
         }
 }
+
+/*
+ * The layer with column-wise scaling factors ("Ours (Acc.)", Sec. 4.2: one
+ * factor per plane and weight column, i.e. per input activation, here a power
+ * of two by Eq. 2) at one output (b, n):
+ *   y       = sum_i sum_k s_i[n][k] * ldexp(x[b][k], e[i][k])
+ *   absterm = sum_i sum_k 2^e[i][k] |x[b][k]|
+ * Loops run planes, then columns, in increasing order.
+ */
+static void one_output_col(const double *xb, const int8_t *signs, const int8_t *col_exps,
+                           int64_t q, int64_t N, int64_t K, int64_t n,
+                           double *y, double *absterm)
+{
+    double total = 0.0, abs_total = 0.0;
+    for (int64_t i = 0; i < q; ++i) {
+        const int8_t *s = signs + (i * N + n) * K;
+        const int8_t *e = col_exps + i * K;
+        for (int64_t k = 0; k < K; ++k) {
+            const double xs = ldexp(xb[k], e[k]);
+            total += (double)s[k] * xs;
+            abs_total += fabs(xs);
+        }
+    }
+    *y = total;
+    *absterm = abs_total;
+}
+
+/* signs: int8 [q][N][K]; col_exps: int8 [q][K]; x: fp64 [B][K]; rows: NULL
+ * for every output row, else the list of rows (nrows of them); y, absterm:
+ * fp64 [B][rows] (absterm may be NULL). */
+void oracle_shiftadd_gemm_colwise(const double *x, const int8_t *signs, const int8_t *col_exps,
+                                  int64_t q, int64_t N, int64_t K, int64_t B,
+                                  const int64_t *rows, int64_t nrows,
+                                  double *y, double *absterm, int nthreads)
+{
+    const int64_t R = rows ? nrows : N;
+    set_threads(nthreads);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < R; ++t) {
+            double v, a;
+            one_output_col(x + b * K, signs, col_exps, q, N, K, rows ? rows[t] : t, &v, &a);
+            y[b * R + t] = v;
+            if (absterm) absterm[b * R + t] = a;
+        }
+}

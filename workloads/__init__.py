@@ -49,6 +49,7 @@ __all__ = [
     "mixed_bits",
     "sha256",
     "fp_weights",
+    "colwise_case",
 ]
 
 
@@ -236,3 +237,22 @@ def fp_weights(N: int, K: int, seed: int = 0, scale: float = 0.02,
         idx = np.unique(rng.integers(0, N * K, size=n_out))
         w.reshape(-1)[idx] *= outlier_scale
     return w.astype(np.float32)
+
+
+def colwise_case(q: int, N: int, K: int, B: int, seed: int = 0,
+                 exp_range: Tuple[int, int] = (-10, -3), outlier_fraction: float = 0.01,
+                 outlier_scale: float = 20.0, copy: int = 0) -> dict:
+    """A seeded layer with column-wise factors ("Acc."): signs [q][N][K] as for
+    the row-wise layers, exponents int8 [q][K] (one per plane and column,
+    uniform over the inclusive range), fp16 activations [B][K] with outlier
+    channels.  Draw order: signs, column exponents, x, outlier channels."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 300, q, N, K, B, copy]))
+    coins = np.unpackbits(rng.integers(0, 256, size=(q, N, K // 8), dtype=np.uint8),
+                          axis=-1, bitorder="little")
+    signs = coins.view(np.int8)
+    signs *= 2
+    signs -= 1
+    col_exps = rng.integers(exp_range[0], exp_range[1] + 1, size=(q, K), dtype=np.int8)
+    x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
+    return dict(signs=signs, col_exps=col_exps, x=x16, outlier_channels=idx, q=q, N=N, K=K,
+                B=B, name=f"colwise(q={q},N={N},K={K},B={B},seed={seed})", seed=seed, copy=copy)
