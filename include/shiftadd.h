@@ -163,7 +163,8 @@ SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int c
 /* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
 typedef struct {
     int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel
-                         (batch 1), 2 batch kernel (batch >= 2) */
+                         (batch 1), 2 batch kernel (batch >= 2); 3: the row kernel
+                         with column-wise factors (sa_shiftadd_gemm_colwise) */
     int rows_per_wg;  /* output rows per workgroup (the largest share when the
                          row kernel spreads row groups unevenly) */
     int workgroups;   /* workgroups of the launch */
@@ -173,6 +174,29 @@ typedef struct {
 } sa_plan;
 
 SA_API int sa_plan_gemm(int q, int N, int K, int group, int batch, sa_plan *plan);
+
+/* The layer with column-wise scaling factors ("Ours (Acc.)", Sec. 4.2): one
+ * power-of-two factor per plane and weight column (Eq. 2, one term, sign
+ * folded into the plane), W_q[n][k] = sum_i 2^col_exps[i][k] s_i[n][k]:
+ *
+ *   y[b][n] = sum_i sum_k s_i[n][k] * 2^col_exps[i][k] * x[b][k]
+ *
+ * A factor belongs to one activation, so it shifts the activation: the tables
+ * of Sec. 4.1 are built per plane from the shifted activations (in fp32,
+ * exact for exponents in [-100, 100]) and the queried sums need no shift.
+ *   x         (device) fp16 bits [batch][K], 16-byte aligned.
+ *   packed_bits (device) planes packed by sa_pack_weights, 16-byte aligned.
+ *   col_exps  (device) int8 [q][K], 8-byte aligned.
+ *   q in [1, 8]; K % 128 == 0 (else SA_ERR_SHAPE); 1 <= batch <= SA_MAX_BATCH.
+ *   y         (device) fp32 [batch][N], 16-byte aligned, fully overwritten.
+ * Same error codes as sa_shiftadd_gemm.  Asynchronous on `stream`; allocates
+ * nothing; deterministic. */
+SA_API int sa_shiftadd_gemm_colwise(const uint16_t *x, const uint8_t *packed_bits,
+                                    const int8_t *col_exps, int q, int N, int K, int batch,
+                                    float *y, void *stream);
+
+/* Launch geometry of sa_shiftadd_gemm_colwise (host-only). */
+SA_API int sa_plan_gemm_colwise(int q, int N, int K, int batch, sa_plan *plan);
 
 /* Measurement aid, not part of the layer (no operation of the paper): reads
  * every byte of `buf` once -- each thread three 16-byte words, grid-strided, so

@@ -239,7 +239,8 @@ static_assert(4 * kRowWaves == kPieceBlocks, "one block per lane per piece");
 struct RowsArgs {
     const uint16_t* x;  // activations [B][K]
     const uint8_t* packed;
-    const int8_t* exps;
+    const int8_t* exps;      // row-wise: [q][N][K/G]
+    const int8_t* col_exps;  // column-wise: [q][K]
     int q, N, K, G, B;
     float* y;           // [B][N]
     int groups;         // 16-row groups of N, spread over the grid
@@ -252,20 +253,24 @@ struct JobRegs {
     uint4 w[Q];
     uint32_t e[Q];  // exponent byte, zero-extended; sign-extended where it is used
     uint4 xr;
+    uint2 xe;       // column-wise: the exponents of the table chunk's 8 columns
 };
 
 // Position of a job inside the workgroup's sequence: row group g (fastest),
-// piece pc, batch row b.
+// piece pc, plane i (column-wise layers only; 0 otherwise), batch row b.
 struct JobPos {
-    int g, pc, b;
+    int g, pc, i, b;
 };
 
-__device__ inline void next_pos(JobPos& j, int nrg, int pieces) {
+__device__ inline void next_pos(JobPos& j, int nrg, int pieces, int planes) {
     if (++j.g == nrg) {
         j.g = 0;
         if (++j.pc == pieces) {
             j.pc = 0;
-            ++j.b;
+            if (++j.i == planes) {
+                j.i = 0;
+                ++j.b;
+            }
         }
     }
 }
@@ -284,13 +289,14 @@ __device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, in
 }
 
 template <int Q>
-__device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, JobRegs<Q>& j) {
+__device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, int plane0,
+                                     JobRegs<Q>& j) {
     const int T = n >> 6;
     const int R = imin(kTileRows, a.N - kTileRows * T);
     const uint32_t off = (uint32_t)(kTileRows * T * C + 16 * (n & 63) + kBlockChunks * J * R);
 #pragma unroll
     for (int i = 0; i < Q; ++i)
-        j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)i * a.N * C + off);
+        j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)(plane0 + i) * a.N * C + off);
 }
 
 // Empty asm that "may modify" one plane's job registers: their consumers
@@ -342,7 +348,11 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
     return tot;
 }
 
-template <int Q, int U>
+// COL: the layer with column-wise factors (one exponent per plane and column).
+// Then a job covers one plane (Q = 1) and the plane is a job dimension; each
+// plane's tables are built from the activations shifted by that plane's
+// column exponents (exact in fp32), and the queried sums need no shift.
+template <int Q, int U, bool COL>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
@@ -354,7 +364,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     const int nrg = base + (wg < extra ? 1 : 0);
     const int rg0 = wg * base + imin(wg, extra);
     const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
-    const int jobs = a.B * pieces * nrg;
+    const int planes = COL ? a.q : 1;
+    const int jobs = a.B * planes * pieces * nrg;
 
     // Slot offsets of this lane's 16 key positions, low and high half (4
     // positions per register, one per byte): byte t of offs[h][wd] is 4*slot
@@ -385,19 +396,31 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     const int my_rho = part >> 1;
     const int slot_lo = 16 * (p & 1) + r;
     const int slot_hi = 32 + slot_lo;
-    // activations of this lane's table chunk
+    // activations of this lane's table chunk (and, column-wise, their
+    // exponents in the job's plane)
+    auto chunk_of = [&](const JobPos& j) {
+        return imin(kPieceChunks * j.pc + kBlockChunks * part + r, C - 1);
+    };
     auto load_x = [&](const JobPos& j) {
-        const int c = imin(kPieceChunks * j.pc + kBlockChunks * part + r, C - 1);
-        return *reinterpret_cast<const uint4*>(a.x + (int64_t)j.b * a.K + 8 * c);
+        return *reinterpret_cast<const uint4*>(a.x + (int64_t)j.b * a.K + 8 * chunk_of(j));
+    };
+    auto load_xe = [&](const JobPos& j) {
+        return *reinterpret_cast<const uint2*>(a.col_exps + (int64_t)j.i * a.K + 8 * chunk_of(j));
     };
     // tables of this wave's four blocks of one piece for one batch row
-    auto build = [&](const uint4 xr) {
+    auto build = [&](const uint4 xr, const uint2 xe) {
         const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
         float f[8];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
             f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
+        }
+        if constexpr (COL) {
+            const uint32_t e2[2] = {xe.x, xe.y};
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                f[t] = ldexpf(f[t], (int)(int8_t)(e2[t >> 2] >> (8 * (t & 3))));
         }
         float lo[16], hi[16];
         nibble_sums(f[0], f[1], f[2], f[3], lo);
@@ -420,11 +443,21 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // then exponents, then keys.
     auto load_job = [&](const JobPos& j, JobRegs<Q>& regs) {
         const int n = row_of(j), J = block_of(j);
-        if (j.g == 0) regs.xr = load_x(j);
-        __builtin_amdgcn_sched_barrier(0);
-        load_job_exps<Q>(a, n, J, NG, bpg, regs);
-        __builtin_amdgcn_sched_barrier(0);
-        load_job_keys<Q>(a, n, J, C, regs);
+        if constexpr (COL) {
+            if (j.g == 0) {
+                regs.xr = load_x(j);
+                regs.xe = load_xe(j);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            regs.e[0] = 0u;
+            load_job_keys<Q>(a, n, J, C, j.i, regs);
+        } else {
+            if (j.g == 0) regs.xr = load_x(j);
+            __builtin_amdgcn_sched_barrier(0);
+            load_job_exps<Q>(a, n, J, NG, bpg, regs);
+            __builtin_amdgcn_sched_barrier(0);
+            load_job_keys<Q>(a, n, J, C, 0, regs);
+        }
     };
     // queries of one job, accumulation into its row group, and -- when the job
     // completes batch row b -- the combination of the 32 lanes of every row
@@ -434,7 +467,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
             if (gg == j.g && valid) acc[gg] += v;
-        if (j.pc == pieces - 1 && j.g == nrg - 1) {
+        if (j.pc == pieces - 1 && j.g == nrg - 1 && j.i == planes - 1) {
 #pragma unroll
             for (int gg = 0; gg < kMaxRG; ++gg) {
                 if (gg < nrg) {
@@ -465,17 +498,17 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // prefetching into a second register set: a loop-carried set of pending
     // loads makes the compiler copy registers at the loop back-edge, which
     // waits for every outstanding load and costs more than it hides.
-    JobPos j{0, 0, 0};
-    if (jobs == 1) {
+    JobPos j{0, 0, 0, 0};
+    if (!COL && jobs == 1) {
         // A single job (a layer of at most 4096 columns and 16 rows per
         // workgroup): every request goes out at once, with no ordering
         // constraint, and the table build waits for the activations only.
         JobRegs<Q> regs;
         regs.xr = load_x(j);
         load_job_exps<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
-        load_job_keys<Q>(a, row_of(j), block_of(j), C, regs);
+        load_job_keys<Q>(a, row_of(j), block_of(j), C, 0, regs);
         __builtin_amdgcn_sched_barrier(0);
-        build(regs.xr);
+        build(regs.xr, regs.xe);
         __builtin_amdgcn_sched_barrier(0);
         run_job(j, regs);
         return;
@@ -493,7 +526,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 #pragma unroll
         for (int u = 1; u < U; ++u) {
             pos[u] = pos[u - 1];
-            if (job + u < jobs) next_pos(pos[u], nrg, pieces);
+            if (job + u < jobs) next_pos(pos[u], nrg, pieces, planes);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) load_job(pos[u], regs[u]);
@@ -501,13 +534,13 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         for (int u = 0; u < U; ++u) {
             if (job + u < jobs) {
                 __builtin_amdgcn_sched_barrier(0);
-                if (pos[u].g == 0) build(regs[u].xr);
+                if (pos[u].g == 0) build(regs[u].xr, regs[u].xe);
                 __builtin_amdgcn_sched_barrier(0);
                 run_job(pos[u], regs[u]);
             }
         }
         j = pos[U - 1];
-        next_pos(j, nrg, pieces);
+        next_pos(j, nrg, pieces, planes);
     }
 }
 
@@ -524,14 +557,22 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4))
 void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>()>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), false>(a, lut, red);
 }
 
 template <int Q>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>()>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), false>(a, lut, red);
+}
+
+// Column-wise factors: one plane per job, registers of a one-plane job.
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_gemm_rows_col(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<1, 1, true>(a, lut, red);
 }
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
@@ -915,6 +956,21 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
+// Column-wise factors: the row kernel with one plane per job (path 3).
+void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
+    (void)q;
+    (void)batch;
+    *p = sa_plan{};
+    const int groups = (N + kGroupRows - 1) / kGroupRows;
+    const int wgs = rows_workgroups(1, N);
+    p->path = 3;
+    p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);
+    p->workgroups = wgs;
+    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
+    p->threads = kRowThreads;
+    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
+}
+
 int launch_status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
 
 int grid_for(int64_t items) {
@@ -1060,6 +1116,44 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
     launch_rows(q, a, plan.workgroups, s);
+    return launch_status();
+}
+
+SA_API int sa_plan_gemm_colwise(int q, int N, int K, int batch, sa_plan* plan) {
+    if (!plan) return SA_ERR_NULL;
+    const int st = check_dims(q, N, K);
+    if (st != SA_OK) return st;
+    if (batch < 1 || batch > SA_MAX_BATCH || (K % 128)) return SA_ERR_SHAPE;
+    make_plan_colwise(q, N, K, batch, plan);
+    return SA_OK;
+}
+
+SA_API int sa_shiftadd_gemm_colwise(const uint16_t* x, const uint8_t* packed_bits,
+                                    const int8_t* col_exps, int q, int N, int K, int batch,
+                                    float* y, void* stream) {
+    if (!x || !packed_bits || !col_exps || !y) return SA_ERR_NULL;
+    const int st = check_dims(q, N, K);
+    if (st != SA_OK) return st;
+    if (batch < 1 || batch > SA_MAX_BATCH || (K % 128)) return SA_ERR_SHAPE;
+    if (!aligned16(x) || !aligned16(packed_bits) || !aligned16(y) ||
+        (reinterpret_cast<uintptr_t>(col_exps) & 7u))
+        return SA_ERR_ALIGN;
+    sa_plan plan;
+    make_plan_colwise(q, N, K, batch, &plan);
+    RowsArgs a{};
+    a.x = x;
+    a.packed = packed_bits;
+    a.exps = nullptr;
+    a.col_exps = col_exps;
+    a.q = q;
+    a.N = N;
+    a.K = K;
+    a.G = K;
+    a.B = batch;
+    a.y = y;
+    a.groups = (N + kGroupRows - 1) / kGroupRows;
+    hipLaunchKernelGGL(k_gemm_rows_col, dim3(plan.workgroups), dim3(kRowThreads), 0,
+                       reinterpret_cast<hipStream_t>(stream), a);
     return launch_status();
 }
 

@@ -171,3 +171,30 @@ def test_quantize_validation_codes():
     assert call(w=A + 8) == sa.SA_ERR_ALIGN   # 16-byte loads
     assert call(s=A + 4) == sa.SA_ERR_ALIGN   # 8-byte stores
     assert call(e=A + 1, w=None) == sa.SA_ERR_NULL  # exps may be unaligned
+
+
+def test_colwise_validation_codes():
+    f = sa.lib.sa_shiftadd_gemm_colwise
+
+    def call(x=A, p=A, e=A, q=3, N=64, K=256, B=1, y=A):
+        return f(x, p, e, q, N, K, B, y, None)
+
+    assert call(x=None) == sa.SA_ERR_NULL
+    assert call(p=None) == sa.SA_ERR_NULL
+    assert call(e=None) == sa.SA_ERR_NULL
+    assert call(y=None) == sa.SA_ERR_NULL
+    assert call(q=0) == sa.SA_ERR_Q
+    assert call(q=9) == sa.SA_ERR_Q
+    assert call(K=200) == sa.SA_ERR_SHAPE   # K % 128 != 0
+    assert call(K=12) == sa.SA_ERR_SHAPE
+    assert call(B=0) == sa.SA_ERR_SHAPE
+    assert call(B=sa.SA_MAX_BATCH + 1) == sa.SA_ERR_SHAPE
+    assert call(x=A + 8) == sa.SA_ERR_ALIGN
+    assert call(p=A + 4) == sa.SA_ERR_ALIGN
+    assert call(y=A + 4) == sa.SA_ERR_ALIGN
+    assert call(e=A + 4) == sa.SA_ERR_ALIGN
+    p = sa.sa_plan_gemm_colwise(3, 4096, 4096, 1)
+    assert p["path"] == 3 and p["workgroups"] == 256 and p["pieces"] == 1
+    assert sa.sa_plan_gemm_colwise(3, 8192, 28672, 1)["pieces"] == 7
+    with pytest.raises(sa.SaError):
+        sa.sa_plan_gemm_colwise(3, 100, 200, 1)

@@ -206,3 +206,24 @@ def test_quantize_full_layer_sampled():
     rel_ref = np.linalg.norm(seg_q - segs) / np.linalg.norm(segs)
     say(f"[bcq] full layer relative error {rel:.4f} (oracle on the sample {rel_ref:.4f})")
     assert rel < 0.5 and abs(rel - rel_ref) < 0.1 * rel_ref
+
+
+def test_quantize_then_layer():
+    """The front-end feeds the layer: quantize on the GPU, pack, run the layer;
+    the result agrees with the oracle's layer on the same planes and with the
+    dense product of the reconstructed weights."""
+    import oracle
+
+    N, K, q, G, T = 512, 1024, 3, 128, 2
+    w = workloads.fp_weights(N, K, seed=21)
+    s_dev, e_dev = sa.quantize_bcq(torch.from_numpy(w).cuda(), q, G, T)
+    packed = sa.pack_weights(s_dev)
+    x = (np.random.default_rng(1).standard_normal((2, K))).astype(np.float16)
+    y = sa.shiftadd_gemm(torch.from_numpy(x).cuda(), packed, e_dev, q, N, K, G)
+    torch.cuda.synchronize()
+    y = y.cpu().numpy().astype(np.float64)
+    s, e = s_dev.cpu().numpy(), e_dev.cpu().numpy()
+    y_ref, a_ref = oracle.shiftadd_gemm(x, s, e, G)
+    assert (np.abs(y - y_ref) / a_ref).max() <= 2e-3
+    y_dense = x.astype(np.float64) @ bcq.reconstruct(s, e, G).T
+    assert np.abs(y_ref - y_dense).max() <= 1e-12 * a_ref.max()
