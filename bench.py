@@ -51,7 +51,7 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch"}
+KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col"}
 
 
 def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
@@ -80,7 +80,14 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
     N = d["N"]
     probe_rows = np.arange(min(N, 256))
     t0 = time.perf_counter()
-    oracle.shiftadd_gemm(d["x"], d["signs"], d["exps"], d["G"], nthreads=threads, rows=probe_rows)
+    def layer(rows):
+        if "col_exps" in d:
+            return oracle.shiftadd_gemm_colwise(d["x"], d["signs"], d["col_exps"],
+                                                nthreads=threads, rows=rows)
+        return oracle.shiftadd_gemm(d["x"], d["signs"], d["exps"], d["G"], nthreads=threads,
+                                    rows=rows)
+
+    layer(probe_rows)
     per_row = (time.perf_counter() - t0) / probe_rows.size
     rows = int(min(N, max(probe_rows.size, seconds / 3 / max(per_row, 1e-9))))
     sel = None if rows >= N else np.linspace(0, N - 1, rows).astype(np.int64)
@@ -88,7 +95,7 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
     deadline = time.perf_counter() + seconds
     while True:
         t0 = time.perf_counter()
-        oracle.shiftadd_gemm(d["x"], d["signs"], d["exps"], d["G"], nthreads=threads, rows=sel)
+        layer(sel)
         times.append(time.perf_counter() - t0)
         if len(times) >= 3 and time.perf_counter() > deadline or len(times) >= 100000:
             break
@@ -314,6 +321,9 @@ def main() -> int:
                     help="only run a plain device copy of this many MB (counter calibration)")
     ap.add_argument("--no-read-floor", action="store_true",
                     help="skip timing a plain read of the layer's bytes (sa_read_probe)")
+    ap.add_argument("--colwise", action="store_true",
+                    help="the layer with column-wise factors (sa_shiftadd_gemm_colwise) on the "
+                         "workload layer's shape")
     ap.add_argument("--quantize", action="store_true",
                     help="time the offline reparameterization (sa_quantize_bcq) instead")
     ap.add_argument("--shape", type=int, nargs=2, default=(4096, 4096), metavar=("N", "K"),
@@ -361,21 +371,36 @@ def main() -> int:
     L = w.layers[args.layer]
     B = args.batch or w.batches[0]
     q, N, K, G = L.q, L.N, L.K, w.group
-    bytes_step = algorithmic_bytes(q, N, K, G, B)
-    weight_bytes = q * N * K // 8 + q * N * (K // G)
+    colwise = args.colwise
+    if colwise:
+        # one exponent per plane and column: q*K exponent bytes
+        bytes_step = algorithmic_bytes(q, N, K, K, B) - q * N + q * K
+        weight_bytes = q * N * K // 8 + q * K
+        plan = sa.sa_plan_gemm_colwise(q, N, K, B)
+    else:
+        bytes_step = algorithmic_bytes(q, N, K, G, B)
+        weight_bytes = q * N * K // 8 + q * N * (K // G)
+        plan = sa.sa_plan_gemm(q, N, K, G, B)
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / weight_bytes))
-    plan = sa.sa_plan_gemm(q, N, K, G, B)
-    log(f"workload {args.workload}/{L.name}: q={q} N={N} K={K} G={G} B={B}; "
-        f"{copies} weight copies ({copies * weight_bytes / 1e6:.0f} MB); plan {plan}")
+    log(f"workload {args.workload}/{L.name}{' column-wise' if colwise else ''}: q={q} N={N} "
+        f"K={K} G={G} B={B}; {copies} weight copies ({copies * weight_bytes / 1e6:.0f} MB); "
+        f"plan {plan}")
 
     t0 = time.perf_counter()
     packed, exps = [], []
     d0 = None
     for c in range(copies):
-        d = workloads.layer_inputs(args.workload, args.layer, B, copy=c)
+        if colwise:
+            d = workloads.colwise_case(q, N, K, B, seed=0, exp_range=w.exp_range,
+                                       outlier_fraction=w.outlier_fraction,
+                                       outlier_scale=w.outlier_scale, copy=c)
+            e = d["col_exps"]
+        else:
+            d = workloads.layer_inputs(args.workload, args.layer, B, copy=c)
+            e = d["exps"]
         s = torch.from_numpy(d["signs"]).cuda()
         packed.append(sa.pack_weights(s))
-        exps.append(torch.from_numpy(d["exps"]).cuda())
+        exps.append(torch.from_numpy(e).cuda())
         del s
         if c == 0:
             d0 = d
@@ -390,7 +415,10 @@ def main() -> int:
 
     def step(i: int) -> None:
         c = i % copies
-        sa.sa_shiftadd_gemm(x, packed[c], exps[c], q, N, K, G, B, y)
+        if colwise:
+            sa.sa_shiftadd_gemm_colwise(x, packed[c], exps[c], q, N, K, B, y)
+        else:
+            sa.sa_shiftadd_gemm(x, packed[c], exps[c], q, N, K, G, B, y)
 
     with torch.cuda.stream(stream):
         for i in range(max(args.warmup, copies)):
@@ -461,7 +489,9 @@ def main() -> int:
         "config": {
             "workload": args.workload,
             "layer": L.name,
-            "N": N, "K": K, "q": q, "group": G, "batch": B,
+            "N": N, "K": K, "q": q, "group": None if colwise else G, "batch": B,
+            "scales": "column-wise (one exponent per plane and column)" if colwise
+                      else f"row-wise, group {G}",
             "weight_copies": copies,
             "launch": "eager" if args.eager else "hip graph replay",
             "kernel": kernel,
