@@ -23,6 +23,10 @@ computes, with the passage it follows:
   column, ``W_q[n][k] = sum_i 2^{e_i[k]} b_i[n][k]``, so that
   ``y = sum_i sum_k b_i[n][k] 2^{e_i[k]} x[k]`` (the factor shifts the
   activation it meets).
+* :func:`shiftadd_gemm_blockwise` -- the layer with block-wise scaling factors
+  ("Ours (Lat.)", Sec. 4.2): 8 columns (one key) and a block of ``row_block``
+  rows share one power-of-two factor,
+  ``y = sum_i sum_c ldexp(sum_{j<8} b_i[n][8c+j] x[8c+j], E[i][n // row_block][c])``.
 """
 from __future__ import annotations
 
@@ -76,6 +80,9 @@ def _load():
     lib.oracle_shiftadd_gemm_colwise.argtypes = [P, P, P, I64, I64, I64, I64, P, I64,
                                                  P, P, ctypes.c_int]
     lib.oracle_shiftadd_gemm_colwise.restype = None
+    lib.oracle_shiftadd_gemm_blockwise.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64,
+                                                   P, P, ctypes.c_int]
+    lib.oracle_shiftadd_gemm_blockwise.restype = None
     _lib = lib
     return lib
 
@@ -190,4 +197,36 @@ def shiftadd_gemm_colwise(x: np.ndarray, signs: np.ndarray, col_exps: np.ndarray
     lib.oracle_shiftadd_gemm_colwise(_ptr(x64), _ptr(signs), _ptr(col_exps), q, N, K, B,
                                      rp, R if r is not None else 0, _ptr(y), _ptr(a),
                                      int(nthreads))
+    return y, a
+
+
+def shiftadd_gemm_blockwise(x: np.ndarray, signs: np.ndarray, blk_exps: np.ndarray,
+                            row_block: int, nthreads: int = 0,
+                            rows: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """``(y, absterm)``, fp64 ``[B][N]`` (or ``[B][len(rows)]``), of the layer with
+    block-wise factors ``E int8 [q][ceil(N / row_block)][K / 8]``:
+    ``y[b][n] = sum_i sum_c ldexp(sum_j s_i[n][8c+j] x[b][8c+j], E[i][n // row_block][c])``."""
+    x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    blk_exps = np.ascontiguousarray(blk_exps, dtype=np.int8)
+    q, N, K = signs.shape
+    B = x64.shape[0]
+    NB = -(-N // row_block)
+    if K % 8 or blk_exps.shape != (q, NB, K // 8):
+        raise ValueError(f"blk_exps shape {blk_exps.shape} != {(q, NB, K // 8)}")
+    if x64.shape != (B, K):
+        raise ValueError(f"x shape {x64.shape} != {(B, K)}")
+    lib = _load()
+    if rows is None:
+        r, R, rp = None, N, None
+    else:
+        r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        if r.size and (r.min() < 0 or r.max() >= N):
+            raise ValueError("row index out of range")
+        R, rp = r.size, _ptr(r)
+    y = np.empty((B, R), dtype=np.float64)
+    a = np.empty((B, R), dtype=np.float64)
+    lib.oracle_shiftadd_gemm_blockwise(_ptr(x64), _ptr(signs), _ptr(blk_exps), q, N, K,
+                                       row_block, B, rp, R if r is not None else 0, _ptr(y),
+                                       _ptr(a), int(nthreads))
     return y, a

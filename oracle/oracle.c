@@ -210,3 +210,55 @@ void oracle_shiftadd_gemm_colwise(const double *x, const int8_t *signs, const in
             if (absterm) absterm[b * R + t] = a;
         }
 }
+
+/*
+ * The layer with block-wise scaling factors ("Ours (Lat.)", Sec. 4.2: 8
+ * columns and a block of rows share one factor, here a power of two by Eq. 2)
+ * at one output (b, n), rows in blocks of row_block:
+ *   y       = sum_i sum_c ldexp( sum_{j<8} s_i[n][8c+j] x[b][8c+j], E[i][n / row_block][c] )
+ *   absterm = sum_i sum_k 2^E[i][n / row_block][k / 8] |x[b][k]|
+ * Loops run planes, then chunks, then columns, in increasing order.
+ */
+static void one_output_blk(const double *xb, const int8_t *signs, const int8_t *blk_exps,
+                           int64_t q, int64_t N, int64_t K, int64_t row_block, int64_t n,
+                           double *y, double *absterm)
+{
+    const int64_t C = K / 8, NB = (N + row_block - 1) / row_block;
+    double total = 0.0, abs_total = 0.0;
+    for (int64_t i = 0; i < q; ++i) {
+        const int8_t *s = signs + (i * N + n) * K;
+        const int8_t *e = blk_exps + (i * NB + n / row_block) * C;
+        for (int64_t c = 0; c < C; ++c) {
+            double part = 0.0, apart = 0.0;
+            for (int64_t k = 8 * c; k < 8 * c + 8; ++k) {
+                part += (double)s[k] * xb[k];
+                apart += fabs(xb[k]);
+            }
+            total += ldexp(part, e[c]);
+            abs_total += ldexp(apart, e[c]);
+        }
+    }
+    *y = total;
+    *absterm = abs_total;
+}
+
+/* signs: int8 [q][N][K]; blk_exps: int8 [q][ceil(N / row_block)][K/8]; x: fp64
+ * [B][K]; rows: NULL for every output row, else nrows rows; y, absterm: fp64
+ * [B][rows] (absterm may be NULL). */
+void oracle_shiftadd_gemm_blockwise(const double *x, const int8_t *signs, const int8_t *blk_exps,
+                                    int64_t q, int64_t N, int64_t K, int64_t row_block, int64_t B,
+                                    const int64_t *rows, int64_t nrows,
+                                    double *y, double *absterm, int nthreads)
+{
+    const int64_t R = rows ? nrows : N;
+    set_threads(nthreads);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < R; ++t) {
+            double v, a;
+            one_output_blk(x + b * K, signs, blk_exps, q, N, K, row_block, rows ? rows[t] : t,
+                           &v, &a);
+            y[b * R + t] = v;
+            if (absterm) absterm[b * R + t] = a;
+        }
+}

@@ -50,6 +50,7 @@ __all__ = [
     "sha256",
     "fp_weights",
     "colwise_case",
+    "blockwise_case",
 ]
 
 
@@ -256,3 +257,26 @@ def colwise_case(q: int, N: int, K: int, B: int, seed: int = 0,
     x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
     return dict(signs=signs, col_exps=col_exps, x=x16, outlier_channels=idx, q=q, N=N, K=K,
                 B=B, name=f"colwise(q={q},N={N},K={K},B={B},seed={seed})", seed=seed, copy=copy)
+
+
+def blockwise_case(q: int, N: int, K: int, B: int, row_block: int, seed: int = 0,
+                   exp_range: Tuple[int, int] = (-10, -3), outlier_fraction: float = 0.01,
+                   outlier_scale: float = 20.0, copy: int = 0) -> dict:
+    """A seeded layer with block-wise factors ("Lat."): signs [q][N][K], one
+    int8 exponent per plane, block of ``row_block`` rows and 8 columns
+    ([q][ceil(N / row_block)][K / 8], uniform over the inclusive range), fp16
+    activations [B][K] with outlier channels.  Draw order: signs, exponents,
+    x, outlier channels."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 400, q, N, K, B, row_block, copy]))
+    coins = np.unpackbits(rng.integers(0, 256, size=(q, N, K // 8), dtype=np.uint8),
+                          axis=-1, bitorder="little")
+    signs = coins.view(np.int8)
+    signs *= 2
+    signs -= 1
+    NB = -(-N // row_block)
+    blk_exps = rng.integers(exp_range[0], exp_range[1] + 1, size=(q, NB, K // 8), dtype=np.int8)
+    x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
+    return dict(signs=signs, blk_exps=blk_exps, row_block=row_block, x=x16,
+                outlier_channels=idx, q=q, N=N, K=K, B=B,
+                name=f"blockwise(q={q},N={N},K={K},B={B},rb={row_block},seed={seed})",
+                seed=seed, copy=copy)
