@@ -164,7 +164,8 @@ SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int c
 typedef struct {
     int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel
                          (batch 1), 2 batch kernel (batch >= 2); 3: the row kernel
-                         with column-wise factors (sa_shiftadd_gemm_colwise) */
+                         with column-wise factors (sa_shiftadd_gemm_colwise); 4: the
+                         row kernel with block-wise factors (sa_shiftadd_gemm_blockwise) */
     int rows_per_wg;  /* output rows per workgroup (the largest share when the
                          row kernel spreads row groups unevenly) */
     int workgroups;   /* workgroups of the launch */
@@ -197,6 +198,27 @@ SA_API int sa_shiftadd_gemm_colwise(const uint16_t *x, const uint8_t *packed_bit
 
 /* Launch geometry of sa_shiftadd_gemm_colwise (host-only). */
 SA_API int sa_plan_gemm_colwise(int q, int N, int K, int batch, sa_plan *plan);
+
+/* The layer with block-wise scaling factors ("Ours (Lat.)", Sec. 4.2): 8
+ * columns (one key) and a block of `row_block` consecutive rows share one
+ * power-of-two factor (Eq. 2, one term, sign folded into the plane):
+ *
+ *   y[b][n] = sum_i sum_c 2^blk_exps[i][n / row_block][c] * sum_{j<8} s_i[n][8c+j] x[b][8c+j]
+ *
+ * One table per chunk serves every plane and row, as in sa_shiftadd_gemm; each
+ * queried entry is shifted by its key's exponent (ldexp) before it is added.
+ * The paper's choice is row_block = N / 8.
+ *   blk_exps  (device) int8 [q][ceil(N / row_block)][K/8], 16-byte aligned.
+ *   row_block >= 1; K % 128 == 0 (else SA_ERR_SHAPE); other arguments as for
+ *   sa_shiftadd_gemm_colwise.
+ * Same error codes as sa_shiftadd_gemm.  Asynchronous on `stream`; allocates
+ * nothing; deterministic. */
+SA_API int sa_shiftadd_gemm_blockwise(const uint16_t *x, const uint8_t *packed_bits,
+                                      const int8_t *blk_exps, int q, int N, int K, int row_block,
+                                      int batch, float *y, void *stream);
+
+/* Launch geometry of sa_shiftadd_gemm_blockwise (host-only). */
+SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch, sa_plan *plan);
 
 /* Measurement aid, not part of the layer (no operation of the paper): reads
  * every byte of `buf` once -- each thread three 16-byte words, grid-strided, so

@@ -9,7 +9,8 @@ __all__ = [
     "sa_packed_bytes", "sa_packed_offset", "sa_pack_weights", "sa_unpack_weights",
     "sa_build_lut", "sa_shiftadd_gemm", "sa_plan_gemm", "sa_shiftadd_gemm_colwise",
     "sa_plan_gemm_colwise", "sa_quantize_bcq", "sa_read_probe", "sa_status_string",
-    "sa_version", "quantize_bcq", "shiftadd_gemm_colwise",
+    "sa_version", "quantize_bcq", "shiftadd_gemm_colwise", "sa_shiftadd_gemm_blockwise",
+    "sa_plan_gemm_blockwise", "shiftadd_gemm_blockwise",
     "pack_weights", "shiftadd_gemm", "SaError",
 ]
 

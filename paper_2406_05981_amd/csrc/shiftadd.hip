@@ -241,10 +241,16 @@ struct RowsArgs {
     const uint8_t* packed;
     const int8_t* exps;      // row-wise: [q][N][K/G]
     const int8_t* col_exps;  // column-wise: [q][K]
+    const int8_t* blk_exps;  // block-wise: [q][NB][K/8], NB = ceil(N / row_block)
     int q, N, K, G, B;
     float* y;           // [B][N]
     int groups;         // 16-row groups of N, spread over the grid
+    int row_block, NB;  // block-wise: rows per block, blocks
 };
+
+// Where the power-of-two factors sit: one per (plane, row, group of G columns),
+// one per (plane, column), or one per (plane, block of rows, 8-column key).
+enum ScaleMode { kRowWise = 0, kColWise = 1, kBlockWise = 2 };
 
 // Keys and exponents of one job for this lane (Q planes of one block), and the
 // activations of the lane's table chunk when the job starts a piece.
@@ -254,6 +260,7 @@ struct JobRegs {
     uint32_t e[Q];  // exponent byte, zero-extended; sign-extended where it is used
     uint4 xr;
     uint2 xe;       // column-wise: the exponents of the table chunk's 8 columns
+    uint4 eb[Q];    // block-wise: the exponents of the block's 16 keys, per plane
 };
 
 // Position of a job inside the workgroup's sequence: row group g (fastest),
@@ -299,6 +306,33 @@ __device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, int
         j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)(plane0 + i) * a.N * C + off);
 }
 
+// Block-wise: the 16 exponents of the lane's 128-column block J in its row's
+// block of rows, per plane (16 bytes; a row of the exponent array is K/8
+// bytes, a multiple of 16).
+template <int Q>
+__device__ inline void load_job_blk_exps(const RowsArgs& a, int n, int J, int C, JobRegs<Q>& j) {
+    const int rb = n / a.row_block;
+#pragma unroll
+    for (int i = 0; i < Q; ++i)
+        j.eb[i] = *reinterpret_cast<const uint4*>(a.blk_exps +
+                                                  ((size_t)i * a.NB + rb) * C + 16 * J);
+}
+
+// Bytes of v rotated so that byte p of the result is byte (p + r) mod 16 of v:
+// the key at position p of a row is chunk (p + r) mod 16 of the block (r = row
+// mod 16), so the rotated exponents line up with the keys.
+__device__ inline void rotate16(const uint4 v, int r, uint32_t out[4]) {
+    const uint32_t in[4] = {v.x, v.y, v.z, v.w};
+    const uint32_t b = (uint32_t)(r & 3);
+    uint32_t t[4], u[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) t[d] = __builtin_amdgcn_alignbyte(in[(d + 1) & 3], in[d], b);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) u[d] = (r & 4) ? t[(d + 1) & 3] : t[d];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) out[d] = (r & 8) ? u[(d + 2) & 3] : u[d];
+}
+
 // Empty asm that "may modify" one plane's job registers: their consumers
 // cannot be hoisted above this point, so the wait for that plane's loads lands
 // here -- after the tables are built and after the previous plane's queries.
@@ -311,15 +345,20 @@ __device__ inline void pin_plane(JobRegs<Q>& j, int i) {
 // Queries and adds of one job: sum over planes of ldexp(block sum, exponent).
 // Planes are consumed in load order, so a plane's queries run while later
 // planes are still arriving.
-template <int Q>
+// Block-wise (BLK): every key has its own exponent, so each queried entry is
+// shifted (ldexp) before it is added and the plane sum needs no shift; r is the
+// lane's row mod 16.
+template <int Q, bool BLK = false>
 __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
-                                const uint32_t offs[2][4], const char* lut_bytes) {
+                                const uint32_t offs[2][4], const char* lut_bytes, int r = 0) {
     float tot = 0.0f;
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
         __builtin_amdgcn_sched_barrier(0);
         pin_plane<Q>(j, i);
         const uint32_t words[4] = {j.w[i].x, j.w[i].y, j.w[i].z, j.w[i].w};
+        uint32_t ek[4];
+        if constexpr (BLK) rotate16(j.eb[i], r, ek);
         float acc;
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
@@ -335,7 +374,13 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
                     lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
                 const float H = *reinterpret_cast<const float*>(
                     lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
-                if (wd == 0 && t == 0) {
+                if constexpr (BLK) {
+                    const float v = ldexpf(L + H, (int)(int8_t)(ek[wd] >> (8 * t)));
+                    if (wd == 0 && t == 0)
+                        acc = v;
+                    else
+                        acc += v;
+                } else if (wd == 0 && t == 0) {
                     acc = L + H;
                 } else {
                     acc += L;
@@ -343,18 +388,25 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
                 }
             }
         }
-        tot += ldexpf(acc, (int)(int8_t)j.e[i]);
+        if constexpr (BLK)
+            tot += acc;
+        else
+            tot += ldexpf(acc, (int)(int8_t)j.e[i]);
     }
     return tot;
 }
 
-// COL: the layer with column-wise factors (one exponent per plane and column).
-// Then a job covers one plane (Q = 1) and the plane is a job dimension; each
-// plane's tables are built from the activations shifted by that plane's
-// column exponents (exact in fp32), and the queried sums need no shift.
-template <int Q, int U, bool COL>
+// MODE kColWise: the layer with column-wise factors (one exponent per plane and
+// column).  Then a job covers one plane (Q = 1) and the plane is a job
+// dimension; each plane's tables are built from the activations shifted by
+// that plane's column exponents (exact in fp32), and the queried sums need no
+// shift.  MODE kBlockWise: one exponent per (plane, block of rows, key); each
+// queried entry is shifted (job_sum).
+template <int Q, int U, int MODE>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
+    constexpr bool COL = MODE == kColWise;
+    constexpr bool BLK = MODE == kBlockWise;
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
@@ -454,7 +506,10 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
         } else {
             if (j.g == 0) regs.xr = load_x(j);
             __builtin_amdgcn_sched_barrier(0);
-            load_job_exps<Q>(a, n, J, NG, bpg, regs);
+            if constexpr (BLK)
+                load_job_blk_exps<Q>(a, n, J, C, regs);
+            else
+                load_job_exps<Q>(a, n, J, NG, bpg, regs);
             __builtin_amdgcn_sched_barrier(0);
             load_job_keys<Q>(a, n, J, C, 0, regs);
         }
@@ -463,7 +518,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // completes batch row b -- the combination of the 32 lanes of every row
     auto run_job = [&](const JobPos& j, JobRegs<Q>& regs) {
         const bool valid = kPieceBlocks * j.pc + part < C16;
-        const float v = job_sum<Q>(regs, rgn_lo, rgn_hi, offs, lut_bytes);
+        const float v = job_sum<Q, BLK>(regs, rgn_lo, rgn_hi, offs, lut_bytes, r);
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
             if (gg == j.g && valid) acc[gg] += v;
@@ -499,7 +554,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // loads makes the compiler copy registers at the loop back-edge, which
     // waits for every outstanding load and costs more than it hides.
     JobPos j{0, 0, 0, 0};
-    if (!COL && jobs == 1) {
+    if (MODE == kRowWise && jobs == 1) {
         // A single job (a layer of at most 4096 columns and 16 rows per
         // workgroup): every request goes out at once, with no ordering
         // constraint, and the table build waits for the activations only.
@@ -557,14 +612,14 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4))
 void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), false>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise>(a, lut, red);
 }
 
 template <int Q>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), false>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise>(a, lut, red);
 }
 
 // Column-wise factors: one plane per job, registers of a one-plane job.
@@ -572,7 +627,23 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4))
 void k_gemm_rows_col(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<1, 1, true>(a, lut, red);
+    gemm_rows_body<1, 1, kColWise>(a, lut, red);
+}
+
+// Block-wise factors: the row kernel with a shift per queried key.
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_gemm_rows_blk(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kBlockWise>(a, lut, red);
+}
+
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) void k_gemm_rows_blk_wide(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kBlockWise>(a, lut, red);
 }
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
@@ -971,6 +1042,13 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
     p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
+// Block-wise factors: the row kernel with a shift per key (path 4).
+void make_plan_blockwise(int q, int N, int K, int batch, sa_plan* p) {
+    make_plan(q, N, K, 128, 1, p);  // the row kernel's geometry
+    (void)batch;
+    p->path = 4;
+}
+
 int launch_status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
 
 int grid_for(int64_t items) {
@@ -1116,6 +1194,55 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
     launch_rows(q, a, plan.workgroups, s);
+    return launch_status();
+}
+
+SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch,
+                                  sa_plan* plan) {
+    if (!plan) return SA_ERR_NULL;
+    const int st = check_dims(q, N, K);
+    if (st != SA_OK) return st;
+    if (batch < 1 || batch > SA_MAX_BATCH || (K % 128) || row_block < 1) return SA_ERR_SHAPE;
+    make_plan_blockwise(q, N, K, batch, plan);
+    return SA_OK;
+}
+
+SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_bits,
+                                      const int8_t* blk_exps, int q, int N, int K, int row_block,
+                                      int batch, float* y, void* stream) {
+    if (!x || !packed_bits || !blk_exps || !y) return SA_ERR_NULL;
+    const int st = check_dims(q, N, K);
+    if (st != SA_OK) return st;
+    if (batch < 1 || batch > SA_MAX_BATCH || (K % 128) || row_block < 1) return SA_ERR_SHAPE;
+    if (!aligned16(x) || !aligned16(packed_bits) || !aligned16(y) || !aligned16(blk_exps))
+        return SA_ERR_ALIGN;
+    sa_plan plan;
+    make_plan_blockwise(q, N, K, batch, &plan);
+    RowsArgs a{};
+    a.x = x;
+    a.packed = packed_bits;
+    a.blk_exps = blk_exps;
+    a.q = q;
+    a.N = N;
+    a.K = K;
+    a.G = K;
+    a.B = batch;
+    a.y = y;
+    a.groups = (N + kGroupRows - 1) / kGroupRows;
+    a.row_block = row_block;
+    a.NB = (N + row_block - 1) / row_block;
+    const dim3 g(plan.workgroups), b(kRowThreads);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    switch (q) {
+        case 1: hipLaunchKernelGGL(k_gemm_rows_blk<1>, g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_gemm_rows_blk<2>, g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(k_gemm_rows_blk<3>, g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_gemm_rows_blk<4>, g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(k_gemm_rows_blk_wide<5>, g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(k_gemm_rows_blk_wide<6>, g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(k_gemm_rows_blk_wide<7>, g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_gemm_rows_blk_wide<8>, g, b, 0, s, a); break;
+    }
     return launch_status();
 }
 

@@ -47,6 +47,8 @@ def _bind(lib):
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_shiftadd_gemm_colwise": ([P, P, P, I, I, I, I, P, P], I),
         "sa_plan_gemm_colwise": ([I, I, I, I, ctypes.POINTER(SaPlan)], I),
+        "sa_shiftadd_gemm_blockwise": ([P, P, P, I, I, I, I, I, P, P], I),
+        "sa_plan_gemm_blockwise": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
         "sa_quantize_bcq": ([P, I, I, I, I, I, P, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
@@ -129,6 +131,13 @@ def sa_plan_gemm_colwise(q: int, N: int, K: int, batch: int) -> dict:
     return {name: getattr(p, name) for name, _ in SaPlan._fields_}
 
 
+def sa_plan_gemm_blockwise(q: int, N: int, K: int, row_block: int, batch: int) -> dict:
+    p = SaPlan()
+    _check(lib.sa_plan_gemm_blockwise(q, N, K, row_block, batch, ctypes.byref(p)),
+           "sa_plan_gemm_blockwise")
+    return {name: getattr(p, name) for name, _ in SaPlan._fields_}
+
+
 def sa_pack_weights(signs: torch.Tensor, q: int, N: int, K: int, packed_bits: torch.Tensor,
                     stream=None) -> None:
     nbytes = sa_packed_bytes(q, N, K)
@@ -179,6 +188,22 @@ def sa_shiftadd_gemm_colwise(x: torch.Tensor, packed_bits: torch.Tensor, col_exp
         _dev(col_exps, "col_exps", torch.int8, q * K),
         q, N, K, batch,
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm_colwise")
+
+
+def sa_shiftadd_gemm_blockwise(x: torch.Tensor, packed_bits: torch.Tensor, blk_exps: torch.Tensor,
+                               q: int, N: int, K: int, row_block: int, batch: int,
+                               y: torch.Tensor, stream=None) -> None:
+    if sa_packed_bytes(q, N, K) == 0:
+        _check(SA_ERR_SHAPE if 1 <= q <= SA_MAX_Q else SA_ERR_Q, "sa_shiftadd_gemm_blockwise")
+    if row_block < 1:
+        _check(SA_ERR_SHAPE, "sa_shiftadd_gemm_blockwise")
+    nb = -(-N // row_block)
+    _check(lib.sa_shiftadd_gemm_blockwise(
+        _dev(x, "x", torch.float16, batch * K),
+        _dev(packed_bits, "packed_bits", torch.uint8, sa_packed_bytes(q, N, K)),
+        _dev(blk_exps, "blk_exps", torch.int8, q * nb * (K // 8)),
+        q, N, K, row_block, batch,
+        _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm_blockwise")
 
 
 def sa_quantize_bcq(w: torch.Tensor, N: int, K: int, q: int, group: int, cycles: int,
@@ -241,4 +266,15 @@ def shiftadd_gemm_colwise(x: torch.Tensor, packed_bits: torch.Tensor, col_exps: 
     batch = x.shape[0] if x.dim() == 2 else 1
     y = out if out is not None else torch.empty((batch, N), dtype=torch.float32, device=x.device)
     sa_shiftadd_gemm_colwise(x, packed_bits, col_exps, q, N, K, batch, y, stream)
+    return y
+
+
+def shiftadd_gemm_blockwise(x: torch.Tensor, packed_bits: torch.Tensor, blk_exps: torch.Tensor,
+                            q: int, N: int, K: int, row_block: int,
+                            out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """``y = x W_q^T`` with block-wise factors, as a new (or the given) fp32
+    ``[batch][N]`` tensor."""
+    batch = x.shape[0] if x.dim() == 2 else 1
+    y = out if out is not None else torch.empty((batch, N), dtype=torch.float32, device=x.device)
+    sa_shiftadd_gemm_blockwise(x, packed_bits, blk_exps, q, N, K, row_block, batch, y, stream)
     return y

@@ -198,3 +198,27 @@ def test_colwise_validation_codes():
     assert sa.sa_plan_gemm_colwise(3, 8192, 28672, 1)["pieces"] == 7
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm_colwise(3, 100, 200, 1)
+
+
+def test_blockwise_validation_codes():
+    f = sa.lib.sa_shiftadd_gemm_blockwise
+
+    def call(x=A, p=A, e=A, q=3, N=64, K=256, rb=8, B=1, y=A):
+        return f(x, p, e, q, N, K, rb, B, y, None)
+
+    assert call(x=None) == sa.SA_ERR_NULL
+    assert call(p=None) == sa.SA_ERR_NULL
+    assert call(e=None) == sa.SA_ERR_NULL
+    assert call(y=None) == sa.SA_ERR_NULL
+    assert call(q=0) == sa.SA_ERR_Q
+    assert call(q=9) == sa.SA_ERR_Q
+    assert call(K=200) == sa.SA_ERR_SHAPE
+    assert call(rb=0) == sa.SA_ERR_SHAPE
+    assert call(B=0) == sa.SA_ERR_SHAPE
+    assert call(x=A + 8) == sa.SA_ERR_ALIGN
+    assert call(e=A + 8) == sa.SA_ERR_ALIGN
+    assert call(y=A + 4) == sa.SA_ERR_ALIGN
+    p = sa.sa_plan_gemm_blockwise(3, 4096, 4096, 512, 1)
+    assert p["path"] == 4 and p["workgroups"] == 256
+    with pytest.raises(sa.SaError):
+        sa.sa_plan_gemm_blockwise(3, 4096, 4096, 0, 1)
