@@ -51,7 +51,8 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col"}
+KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col",
+           4: "k_gemm_rows_blk"}
 
 
 def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
@@ -81,6 +82,9 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
     probe_rows = np.arange(min(N, 256))
     t0 = time.perf_counter()
     def layer(rows):
+        if "blk_exps" in d:
+            return oracle.shiftadd_gemm_blockwise(d["x"], d["signs"], d["blk_exps"],
+                                                  d["row_block"], nthreads=threads, rows=rows)
         if "col_exps" in d:
             return oracle.shiftadd_gemm_colwise(d["x"], d["signs"], d["col_exps"],
                                                 nthreads=threads, rows=rows)
@@ -324,6 +328,9 @@ def main() -> int:
     ap.add_argument("--colwise", action="store_true",
                     help="the layer with column-wise factors (sa_shiftadd_gemm_colwise) on the "
                          "workload layer's shape")
+    ap.add_argument("--blockwise", action="store_true",
+                    help="the layer with block-wise factors (sa_shiftadd_gemm_blockwise, blocks "
+                         "of 8 columns x N/8 rows) on the workload layer's shape")
     ap.add_argument("--quantize", action="store_true",
                     help="time the offline reparameterization (sa_quantize_bcq) instead")
     ap.add_argument("--shape", type=int, nargs=2, default=(4096, 4096), metavar=("N", "K"),
@@ -371,8 +378,14 @@ def main() -> int:
     L = w.layers[args.layer]
     B = args.batch or w.batches[0]
     q, N, K, G = L.q, L.N, L.K, w.group
-    colwise = args.colwise
-    if colwise:
+    colwise, blockwise = args.colwise, args.blockwise
+    rb = (N + 7) // 8  # block-wise: the paper's blocks of N/8 rows
+    nb = (N + rb - 1) // rb
+    if blockwise:
+        bytes_step = algorithmic_bytes(q, N, K, K, B) - q * N + q * nb * (K // 8)
+        weight_bytes = q * N * K // 8 + q * nb * (K // 8)
+        plan = sa.sa_plan_gemm_blockwise(q, N, K, rb, B)
+    elif colwise:
         # one exponent per plane and column: q*K exponent bytes
         bytes_step = algorithmic_bytes(q, N, K, K, B) - q * N + q * K
         weight_bytes = q * N * K // 8 + q * K
@@ -382,7 +395,8 @@ def main() -> int:
         weight_bytes = q * N * K // 8 + q * N * (K // G)
         plan = sa.sa_plan_gemm(q, N, K, G, B)
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / weight_bytes))
-    log(f"workload {args.workload}/{L.name}{' column-wise' if colwise else ''}: q={q} N={N} "
+    mode = " column-wise" if colwise else (" block-wise" if blockwise else "")
+    log(f"workload {args.workload}/{L.name}{mode}: q={q} N={N} "
         f"K={K} G={G} B={B}; {copies} weight copies ({copies * weight_bytes / 1e6:.0f} MB); "
         f"plan {plan}")
 
@@ -390,7 +404,12 @@ def main() -> int:
     packed, exps = [], []
     d0 = None
     for c in range(copies):
-        if colwise:
+        if blockwise:
+            d = workloads.blockwise_case(q, N, K, B, rb, seed=0, exp_range=w.exp_range,
+                                         outlier_fraction=w.outlier_fraction,
+                                         outlier_scale=w.outlier_scale, copy=c)
+            e = d["blk_exps"]
+        elif colwise:
             d = workloads.colwise_case(q, N, K, B, seed=0, exp_range=w.exp_range,
                                        outlier_fraction=w.outlier_fraction,
                                        outlier_scale=w.outlier_scale, copy=c)
@@ -415,7 +434,9 @@ def main() -> int:
 
     def step(i: int) -> None:
         c = i % copies
-        if colwise:
+        if blockwise:
+            sa.sa_shiftadd_gemm_blockwise(x, packed[c], exps[c], q, N, K, rb, B, y)
+        elif colwise:
             sa.sa_shiftadd_gemm_colwise(x, packed[c], exps[c], q, N, K, B, y)
         else:
             sa.sa_shiftadd_gemm(x, packed[c], exps[c], q, N, K, G, B, y)
@@ -489,9 +510,10 @@ def main() -> int:
         "config": {
             "workload": args.workload,
             "layer": L.name,
-            "N": N, "K": K, "q": q, "group": None if colwise else G, "batch": B,
-            "scales": "column-wise (one exponent per plane and column)" if colwise
-                      else f"row-wise, group {G}",
+            "N": N, "K": K, "q": q, "group": None if colwise or blockwise else G, "batch": B,
+            "scales": ("column-wise (one exponent per plane and column)" if colwise else
+                       f"block-wise (8 columns x {rb} rows)" if blockwise else
+                       f"row-wise, group {G}"),
             "weight_copies": copies,
             "launch": "eager" if args.eager else "hip graph replay",
             "kernel": kernel,
