@@ -27,6 +27,9 @@ computes, with the passage it follows:
   ("Ours (Lat.)", Sec. 4.2): 8 columns (one key) and a block of ``row_block``
   rows share one power-of-two factor,
   ``y = sum_i sum_c ldexp(sum_{j<8} b_i[n][8c+j] x[8c+j], E[i][n // row_block][c])``.
+* :func:`shiftadd_gemm_terms` -- the layer with additive power-of-two factors
+  (Eq. 2 with T terms): the factor of (plane, row, group) is
+  ``sum_t sg_t 2^{e_t}``, term signs in {-1, 0, +1} (0: no term).
 """
 from __future__ import annotations
 
@@ -83,6 +86,9 @@ def _load():
     lib.oracle_shiftadd_gemm_blockwise.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64,
                                                    P, P, ctypes.c_int]
     lib.oracle_shiftadd_gemm_blockwise.restype = None
+    lib.oracle_shiftadd_gemm_terms.argtypes = [P, P, P, P, I64, I64, I64, I64, I64, I64, P,
+                                               I64, P, P, ctypes.c_int]
+    lib.oracle_shiftadd_gemm_terms.restype = None
     _lib = lib
     return lib
 
@@ -229,4 +235,38 @@ def shiftadd_gemm_blockwise(x: np.ndarray, signs: np.ndarray, blk_exps: np.ndarr
     lib.oracle_shiftadd_gemm_blockwise(_ptr(x64), _ptr(signs), _ptr(blk_exps), q, N, K,
                                        row_block, B, rp, R if r is not None else 0, _ptr(y),
                                        _ptr(a), int(nthreads))
+    return y, a
+
+
+def shiftadd_gemm_terms(x: np.ndarray, signs: np.ndarray, exps: np.ndarray,
+                        term_signs: np.ndarray, G: int, nthreads: int = 0,
+                        rows: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """``(y, absterm)`` of the layer with additive power-of-two factors:
+    ``exps, term_signs int8 [T][q][N][K/G]``,
+    ``y[b][n] = sum_i sum_g sum_t sg_t ldexp(sum_{k in g} s_i[n][k] x[b][k], e_t)``."""
+    x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    exps = np.ascontiguousarray(exps, dtype=np.int8)
+    term_signs = np.ascontiguousarray(term_signs, dtype=np.int8)
+    q, N, K = signs.shape
+    B = x64.shape[0]
+    T = exps.shape[0]
+    if K % 8 or G % 8 or K % G or exps.shape != (T, q, N, K // G) or term_signs.shape != exps.shape:
+        raise ValueError(f"exps/term_signs shape {exps.shape}/{term_signs.shape} != "
+                         f"{(T, q, N, K // G)}")
+    if x64.shape != (B, K):
+        raise ValueError(f"x shape {x64.shape} != {(B, K)}")
+    lib = _load()
+    if rows is None:
+        r, R, rp = None, N, None
+    else:
+        r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        if r.size and (r.min() < 0 or r.max() >= N):
+            raise ValueError("row index out of range")
+        R, rp = r.size, _ptr(r)
+    y = np.empty((B, R), dtype=np.float64)
+    a = np.empty((B, R), dtype=np.float64)
+    lib.oracle_shiftadd_gemm_terms(_ptr(x64), _ptr(signs), _ptr(exps), _ptr(term_signs), T, q,
+                                   N, K, G, B, rp, R if r is not None else 0, _ptr(y), _ptr(a),
+                                   int(nthreads))
     return y, a

@@ -262,3 +262,58 @@ void oracle_shiftadd_gemm_blockwise(const double *x, const int8_t *signs, const 
             if (absterm) absterm[b * R + t] = a;
         }
 }
+
+/*
+ * The layer with additive power-of-two factors (Eq. 2 with T terms): the
+ * factor of (plane i, row n, group g) is sum_t sg[t][i][n][g] 2^e[t][i][n][g]
+ * with term signs in {-1, 0, +1} (0: no term), so that
+ *   y       = sum_i sum_g sum_t sg_t ldexp( sum_{k in g} s_i[n][k] x[b][k], e_t )
+ *   absterm = sum_i sum_g sum_t |sg_t| ldexp( sum_{k in g} |x[b][k]|, e_t )
+ * Loops run planes, then groups, then terms, then columns.
+ */
+static void one_output_terms(const double *xb, const int8_t *signs, const int8_t *exps,
+                             const int8_t *term_signs, int64_t T, int64_t q, int64_t N,
+                             int64_t K, int64_t G, int64_t n, double *y, double *absterm)
+{
+    const int64_t NG = K / G, plane = q * N * NG;
+    double total = 0.0, abs_total = 0.0;
+    for (int64_t i = 0; i < q; ++i) {
+        const int8_t *s = signs + (i * N + n) * K;
+        for (int64_t g = 0; g < NG; ++g) {
+            double part = 0.0, apart = 0.0;
+            for (int64_t k = g * G; k < (g + 1) * G; ++k) {
+                part += (double)s[k] * xb[k];
+                apart += fabs(xb[k]);
+            }
+            const int64_t at = (i * N + n) * NG + g;
+            for (int64_t t = 0; t < T; ++t) {
+                const int sg = term_signs[t * plane + at];
+                if (sg == 0) continue;
+                total += (double)sg * ldexp(part, exps[t * plane + at]);
+                abs_total += ldexp(apart, exps[t * plane + at]);
+            }
+        }
+    }
+    *y = total;
+    *absterm = abs_total;
+}
+
+/* exps, term_signs: int8 [T][q][N][K/G]; other arguments as
+ * oracle_shiftadd_gemm_blockwise. */
+void oracle_shiftadd_gemm_terms(const double *x, const int8_t *signs, const int8_t *exps,
+                                const int8_t *term_signs, int64_t T, int64_t q, int64_t N,
+                                int64_t K, int64_t G, int64_t B, const int64_t *rows,
+                                int64_t nrows, double *y, double *absterm, int nthreads)
+{
+    const int64_t R = rows ? nrows : N;
+    set_threads(nthreads);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < R; ++t) {
+            double v, a;
+            one_output_terms(x + b * K, signs, exps, term_signs, T, q, N, K, G,
+                             rows ? rows[t] : t, &v, &a);
+            y[b * R + t] = v;
+            if (absterm) absterm[b * R + t] = a;
+        }
+}

@@ -51,6 +51,7 @@ __all__ = [
     "fp_weights",
     "colwise_case",
     "blockwise_case",
+    "terms_case",
 ]
 
 
@@ -279,4 +280,35 @@ def blockwise_case(q: int, N: int, K: int, B: int, row_block: int, seed: int = 0
     return dict(signs=signs, blk_exps=blk_exps, row_block=row_block, x=x16,
                 outlier_channels=idx, q=q, N=N, K=K, B=B,
                 name=f"blockwise(q={q},N={N},K={K},B={B},rb={row_block},seed={seed})",
+                seed=seed, copy=copy)
+
+
+def terms_case(q: int, N: int, K: int, G: int, B: int, T: int, seed: int = 0,
+               exp_range: Tuple[int, int] = (-10, -3), outlier_fraction: float = 0.01,
+               outlier_scale: float = 20.0, copy: int = 0) -> dict:
+    """A seeded layer with additive power-of-two factors (Eq. 2, T terms):
+    signs [q][N][K]; exps int8 [T][q][N][K/G] where term t is drawn below the
+    previous one (term 0 uniform over the range, term t = term t-1 minus 1..3,
+    as a greedy residual expansion would give); term signs int8 [T][q][N][K/G]:
+    term 0 is +1 (its sign is folded into the plane), later terms are +-1 or, one
+    time in eight, 0 (no term).  Draw order: signs, exps, term signs, x,
+    outlier channels."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 500, q, N, K, G, B, T, copy]))
+    coins = np.unpackbits(rng.integers(0, 256, size=(q, N, K // 8), dtype=np.uint8),
+                          axis=-1, bitorder="little")
+    signs = coins.view(np.int8)
+    signs *= 2
+    signs -= 1
+    NG = K // G
+    e0 = rng.integers(exp_range[0], exp_range[1] + 1, size=(q, N, NG))
+    exps = np.empty((T, q, N, NG), dtype=np.int8)
+    exps[0] = e0
+    for t in range(1, T):
+        e0 = e0 - rng.integers(1, 4, size=(q, N, NG))
+        exps[t] = e0
+    tsg = rng.choice(np.array([-1, 1, 1, 1, -1, 1, -1, 0], dtype=np.int8), size=(T, q, N, NG))
+    tsg[0] = 1
+    x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
+    return dict(signs=signs, exps=exps, term_signs=tsg, x=x16, outlier_channels=idx, q=q, N=N,
+                K=K, G=G, B=B, T=T, name=f"terms(q={q},N={N},K={K},G={G},B={B},T={T})",
                 seed=seed, copy=copy)
