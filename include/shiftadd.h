@@ -66,6 +66,7 @@ typedef enum {
 #define SA_MAX_Q 8
 #define SA_MAX_BATCH 256
 #define SA_MAX_CYCLES 64
+#define SA_MAX_TERMS 4
 
 /* Bytes of the packed planes of a q x N x K layer: q*N*K/8 (1 bit per weight
  * per plane, no padding).  Returns 0 for invalid sizes. */
@@ -216,6 +217,23 @@ SA_API int sa_plan_gemm_colwise(int q, int N, int K, int batch, sa_plan *plan);
 SA_API int sa_shiftadd_gemm_blockwise(const uint16_t *x, const uint8_t *packed_bits,
                                       const int8_t *blk_exps, int q, int N, int K, int row_block,
                                       int batch, float *y, void *stream);
+
+/* The layer with additive power-of-two factors (Eq. 2 with T terms): the
+ * factor of (plane i, row n, group g) is the greedy sum of T signed powers of
+ * two, sum_t term_signs[t] 2^exps[t] (a term sign of 0 means no term):
+ *
+ *   y[b][n] = sum_i sum_g ( sum_t term_signs[t][i][n][g] 2^exps[t][i][n][g] )
+ *                         * sum_{k in g} s_i[n][k] x[b][k]
+ *
+ * Each group sum is shifted once per term and added with its sign.  T = 1
+ * with term sign +1 is sa_shiftadd_gemm.
+ *   exps, term_signs (device) int8 [T][q][N][K/group], term signs in {-1, 0, 1}.
+ *   group % 128 == 0 (else SA_ERR_GROUP); 1 <= terms <= SA_MAX_TERMS (else
+ *   SA_ERR_SHAPE); other arguments and errors as for sa_shiftadd_gemm.
+ * Asynchronous on `stream`; allocates nothing; deterministic. */
+SA_API int sa_shiftadd_gemm_terms(const uint16_t *x, const uint8_t *packed_bits,
+                                  const int8_t *exps, const int8_t *term_signs, int q, int N,
+                                  int K, int group, int terms, int batch, float *y, void *stream);
 
 /* Launch geometry of sa_shiftadd_gemm_blockwise (host-only). */
 SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch, sa_plan *plan);

@@ -10,7 +10,7 @@ __all__ = [
     "sa_build_lut", "sa_shiftadd_gemm", "sa_plan_gemm", "sa_shiftadd_gemm_colwise",
     "sa_plan_gemm_colwise", "sa_quantize_bcq", "sa_read_probe", "sa_status_string",
     "sa_version", "quantize_bcq", "shiftadd_gemm_colwise", "sa_shiftadd_gemm_blockwise",
-    "sa_plan_gemm_blockwise", "shiftadd_gemm_blockwise",
+    "sa_plan_gemm_blockwise", "shiftadd_gemm_blockwise", "sa_shiftadd_gemm_terms",
     "pack_weights", "shiftadd_gemm", "SaError",
 ]
 

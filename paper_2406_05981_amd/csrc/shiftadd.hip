@@ -246,11 +246,15 @@ struct RowsArgs {
     float* y;           // [B][N]
     int groups;         // 16-row groups of N, spread over the grid
     int row_block, NB;  // block-wise: rows per block, blocks
+    const int8_t* term_signs;  // additive: [T][q][N][K/G], with exps [T][q][N][K/G]
+    int terms;                 // additive: T
 };
 
 // Where the power-of-two factors sit: one per (plane, row, group of G columns),
-// one per (plane, column), or one per (plane, block of rows, 8-column key).
-enum ScaleMode { kRowWise = 0, kColWise = 1, kBlockWise = 2 };
+// one per (plane, column), one per (plane, block of rows, 8-column key), or a
+// sum of T signed terms per (plane, row, group) (additive, Eq. 2).
+enum ScaleMode { kRowWise = 0, kColWise = 1, kBlockWise = 2, kAdditive = 3 };
+constexpr int kMaxTerms = 4;
 
 // Keys and exponents of one job for this lane (Q planes of one block), and the
 // activations of the lane's table chunk when the job starts a piece.
@@ -261,6 +265,8 @@ struct JobRegs {
     uint4 xr;
     uint2 xe;       // column-wise: the exponents of the table chunk's 8 columns
     uint4 eb[Q];    // block-wise: the exponents of the block's 16 keys, per plane
+    uint32_t et[Q]; // additive: the T exponent bytes of the plane's group, one per byte
+    uint32_t st[Q]; // additive: the T term signs, one per byte
 };
 
 // Position of a job inside the workgroup's sequence: row group g (fastest),
@@ -306,6 +312,28 @@ __device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, int
         j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)(plane0 + i) * a.N * C + off);
 }
 
+// Additive: the T exponents and term signs of the lane's group in every plane.
+template <int Q>
+__device__ inline void load_job_terms(const RowsArgs& a, int n, int J, int NG, int bpg,
+                                      JobRegs<Q>& j) {
+    const uint32_t off = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg));
+    const size_t term_stride = (size_t)a.q * a.N * NG;
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+        uint32_t e = 0, sg = 0;
+#pragma unroll
+        for (int t = 0; t < kMaxTerms; ++t) {
+            if (t < a.terms) {
+                const size_t at = t * term_stride + (size_t)i * a.N * NG + off;
+                e |= (uint32_t)reinterpret_cast<const uint8_t*>(a.exps)[at] << (8 * t);
+                sg |= (uint32_t)reinterpret_cast<const uint8_t*>(a.term_signs)[at] << (8 * t);
+            }
+        }
+        j.et[i] = e;
+        j.st[i] = sg;
+    }
+}
+
 // Block-wise: the 16 exponents of the lane's 128-column block J in its row's
 // block of rows, per plane (16 bytes; a row of the exponent array is K/8
 // bytes, a multiple of 16).
@@ -347,10 +375,12 @@ __device__ inline void pin_plane(JobRegs<Q>& j, int i) {
 // planes are still arriving.
 // Block-wise (BLK): every key has its own exponent, so each queried entry is
 // shifted (ldexp) before it is added and the plane sum needs no shift; r is the
-// lane's row mod 16.
+// lane's row mod 16.  Additive (terms > 0): the plane sum is shifted once per
+// term and added with the term's sign (0: no term).
 template <int Q, bool BLK = false>
 __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
-                                const uint32_t offs[2][4], const char* lut_bytes, int r = 0) {
+                                const uint32_t offs[2][4], const char* lut_bytes, int r = 0,
+                                int terms = 0) {
     float tot = 0.0f;
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
@@ -388,10 +418,20 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
                 }
             }
         }
-        if constexpr (BLK)
+        if constexpr (BLK) {
             tot += acc;
-        else
+        } else if (terms > 0) {
+#pragma unroll
+            for (int t = 0; t < kMaxTerms; ++t) {
+                const int sg = (int)(int8_t)(j.st[i] >> (8 * t));
+                if (t < terms && sg != 0) {
+                    const float v = ldexpf(acc, (int)(int8_t)(j.et[i] >> (8 * t)));
+                    tot += sg < 0 ? -v : v;
+                }
+            }
+        } else {
             tot += ldexpf(acc, (int)(int8_t)j.e[i]);
+        }
     }
     return tot;
 }
@@ -407,6 +447,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     constexpr bool COL = MODE == kColWise;
     constexpr bool BLK = MODE == kBlockWise;
+    constexpr bool ADD = MODE == kAdditive;
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
@@ -508,6 +549,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (BLK)
                 load_job_blk_exps<Q>(a, n, J, C, regs);
+            else if constexpr (ADD)
+                load_job_terms<Q>(a, n, J, NG, bpg, regs);
             else
                 load_job_exps<Q>(a, n, J, NG, bpg, regs);
             __builtin_amdgcn_sched_barrier(0);
@@ -518,7 +561,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // completes batch row b -- the combination of the 32 lanes of every row
     auto run_job = [&](const JobPos& j, JobRegs<Q>& regs) {
         const bool valid = kPieceBlocks * j.pc + part < C16;
-        const float v = job_sum<Q, BLK>(regs, rgn_lo, rgn_hi, offs, lut_bytes, r);
+        const float v = job_sum<Q, BLK>(regs, rgn_lo, rgn_hi, offs, lut_bytes, r,
+                                        ADD ? a.terms : 0);
 #pragma unroll
         for (int gg = 0; gg < kMaxRG; ++gg)
             if (gg == j.g && valid) acc[gg] += v;
@@ -644,6 +688,22 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_blk_wide(RowsArgs a) 
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
     gemm_rows_body<Q, 1, kBlockWise>(a, lut, red);
+}
+
+// Additive factors: the row kernel with T signed shifts per plane sum.
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_gemm_rows_add(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kAdditive>(a, lut, red);
+}
+
+template <int Q>
+__global__ __launch_bounds__(kRowThreads) void k_gemm_rows_add_wide(RowsArgs a) {
+    __shared__ float lut[16 * kRegionFloats];  // 64 KB
+    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kAdditive>(a, lut, red);
 }
 
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
@@ -1242,6 +1302,45 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
         case 6: hipLaunchKernelGGL(k_gemm_rows_blk_wide<6>, g, b, 0, s, a); break;
         case 7: hipLaunchKernelGGL(k_gemm_rows_blk_wide<7>, g, b, 0, s, a); break;
         default: hipLaunchKernelGGL(k_gemm_rows_blk_wide<8>, g, b, 0, s, a); break;
+    }
+    return launch_status();
+}
+
+SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
+                                  const int8_t* exps, const int8_t* term_signs, int q, int N,
+                                  int K, int group, int terms, int batch, float* y,
+                                  void* stream) {
+    if (!term_signs) return SA_ERR_NULL;
+    const int st = validate_gemm(x, packed_bits, exps, q, N, K, group, batch, y);
+    if (st != SA_OK) return st;
+    if (group % 128) return SA_ERR_GROUP;
+    if (terms < 1 || terms > SA_MAX_TERMS) return SA_ERR_SHAPE;
+    sa_plan plan;
+    make_plan(q, N, K, group, 1, &plan);  // the row kernel's geometry
+    RowsArgs a{};
+    a.x = x;
+    a.packed = packed_bits;
+    a.exps = exps;
+    a.term_signs = term_signs;
+    a.terms = terms;
+    a.q = q;
+    a.N = N;
+    a.K = K;
+    a.G = group;
+    a.B = batch;
+    a.y = y;
+    a.groups = (N + kGroupRows - 1) / kGroupRows;
+    const dim3 g(plan.workgroups), b(kRowThreads);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    switch (q) {
+        case 1: hipLaunchKernelGGL(k_gemm_rows_add<1>, g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_gemm_rows_add<2>, g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(k_gemm_rows_add<3>, g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_gemm_rows_add<4>, g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(k_gemm_rows_add_wide<5>, g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(k_gemm_rows_add_wide<6>, g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(k_gemm_rows_add_wide<7>, g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_gemm_rows_add_wide<8>, g, b, 0, s, a); break;
     }
     return launch_status();
 }

@@ -49,6 +49,7 @@ def _bind(lib):
         "sa_plan_gemm_colwise": ([I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_shiftadd_gemm_blockwise": ([P, P, P, I, I, I, I, I, P, P], I),
         "sa_plan_gemm_blockwise": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
+        "sa_shiftadd_gemm_terms": ([P, P, P, P, I, I, I, I, I, I, P, P], I),
         "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
         "sa_quantize_bcq": ([P, I, I, I, I, I, P, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
@@ -68,6 +69,7 @@ SA_OK, SA_ERR_NULL, SA_ERR_SHAPE, SA_ERR_Q, SA_ERR_GROUP, SA_ERR_ALIGN, SA_ERR_H
 SA_MAX_Q = 8
 SA_MAX_BATCH = 256
 SA_MAX_CYCLES = 64
+SA_MAX_TERMS = 4
 
 
 class SaError(RuntimeError):
@@ -204,6 +206,24 @@ def sa_shiftadd_gemm_blockwise(x: torch.Tensor, packed_bits: torch.Tensor, blk_e
         _dev(blk_exps, "blk_exps", torch.int8, q * nb * (K // 8)),
         q, N, K, row_block, batch,
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm_blockwise")
+
+
+def sa_shiftadd_gemm_terms(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Tensor,
+                           term_signs: torch.Tensor, q: int, N: int, K: int, group: int,
+                           terms: int, batch: int, y: torch.Tensor, stream=None) -> None:
+    if sa_packed_bytes(q, N, K) == 0:
+        _check(SA_ERR_SHAPE if 1 <= q <= SA_MAX_Q else SA_ERR_Q, "sa_shiftadd_gemm_terms")
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_shiftadd_gemm_terms")
+    if terms < 1 or terms > SA_MAX_TERMS:
+        _check(SA_ERR_SHAPE, "sa_shiftadd_gemm_terms")
+    n_e = terms * q * N * (K // group)
+    _check(lib.sa_shiftadd_gemm_terms(
+        _dev(x, "x", torch.float16, batch * K),
+        _dev(packed_bits, "packed_bits", torch.uint8, sa_packed_bytes(q, N, K)),
+        _dev(exps, "exps", torch.int8, n_e), _dev(term_signs, "term_signs", torch.int8, n_e),
+        q, N, K, group, terms, batch,
+        _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm_terms")
 
 
 def sa_quantize_bcq(w: torch.Tensor, N: int, K: int, q: int, group: int, cycles: int,

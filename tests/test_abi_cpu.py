@@ -222,3 +222,20 @@ def test_blockwise_validation_codes():
     assert p["path"] == 4 and p["workgroups"] == 256
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm_blockwise(3, 4096, 4096, 0, 1)
+
+
+def test_terms_validation_codes():
+    f = sa.lib.sa_shiftadd_gemm_terms
+
+    def call(x=A, p=A, e=A, s=A, q=3, N=64, K=256, G=128, T=2, B=1, y=A):
+        return f(x, p, e, s, q, N, K, G, T, B, y, None)
+
+    assert call(s=None) == sa.SA_ERR_NULL
+    assert call(e=None) == sa.SA_ERR_NULL
+    assert call(x=None) == sa.SA_ERR_NULL
+    assert call(q=9) == sa.SA_ERR_Q
+    assert call(G=64) == sa.SA_ERR_GROUP    # the row kernel takes groups of 128 columns
+    assert call(G=96) == sa.SA_ERR_GROUP
+    assert call(T=0) == sa.SA_ERR_SHAPE
+    assert call(T=sa.SA_MAX_TERMS + 1) == sa.SA_ERR_SHAPE
+    assert call(x=A + 8) == sa.SA_ERR_ALIGN

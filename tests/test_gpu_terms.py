@@ -1,0 +1,94 @@
+"""GPU parity of the layer with additive power-of-two factors
+(sa_shiftadd_gemm_terms, Eq. 2 with T terms) against the CPU oracle
+(oracle.shiftadd_gemm_terms).
+
+Bar (fixed here): max |y - y_ref| / sum|terms| <= 2e-3 per output, with the
+1e-5 alarm of the fp32 tables (each term is an exact shift of the fp32 group
+sum)."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only environment
+    pytest.skip("no GPU", allow_module_level=True)
+sa = pytest.importorskip("paper_2406_05981_amd.shiftadd")
+
+TOL = 2e-3
+ALARM = 1e-5
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def run(c):
+    q, N, K, G, B, T = c["q"], c["N"], c["K"], c["G"], c["B"], c["T"]
+    y = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm_terms(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"]),
+                              dev(c["term_signs"]), q, N, K, G, T, B, y)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+def check(y, y_ref, a_ref, what):
+    assert np.isfinite(y).all(), what
+    err = np.abs(y - y_ref)
+    zero = a_ref == 0
+    assert (err[zero] == 0).all(), what
+    worst = float((err[~zero] / a_ref[~zero]).max()) if (~zero).any() else 0.0
+    say(f"  {what}: max |y-y_ref|/sum|terms| = {worst:.3e}")
+    assert worst <= TOL and worst <= ALARM, what
+
+
+CASES = [
+    # (q, N, K, G, B, T, label)
+    (3, 768, 768, 128, 1, 2, "two terms, one piece"),
+    (2, 130, 384, 384, 1, 3, "G = K, ragged rows, three terms"),
+    (1, 33, 128, 128, 3, 4, "four terms, batch 3"),
+    (4, 4100, 1024, 256, 2, 2, "G = 256, several row groups per workgroup"),
+    (3, 64, 8192, 128, 1, 3, "two pieces"),
+    (8, 17, 256, 128, 1, 2, "eight planes"),
+    (3, 300, 4224, 128, 2, 4, "ragged last piece"),
+]
+
+
+@pytest.mark.parametrize("q,N,K,G,B,T,label", CASES, ids=[c[-1] for c in CASES])
+def test_terms_parity(q, N, K, G, B, T, label):
+    say(f"terms q={q} N={N} K={K} G={G} B={B} T={T}: {label}")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=q + N + K + B + T)
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G)
+    check(y, y_ref, a_ref, label)
+
+
+def test_one_term_matches_row_wise_kernel():
+    q, N, K, G, B = 3, 512, 2048, 128, 1
+    c = workloads.terms_case(q, N, K, G, B, 1, seed=11)
+    y = run(c)
+    yr = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"][0]), q, N,
+                        K, G, B, yr)
+    torch.cuda.synchronize()
+    assert np.array_equal(y, yr.cpu().numpy().astype(np.float64))  # same arithmetic
+
+
+def test_terms_full_size_sampled():
+    q, N, K, G, B, T = 3, 4096, 4096, 128, 1, 2
+    say("terms full size 4096x4096 T=2")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=1)
+    y = run(c)
+    rows = np.sort(np.random.default_rng(0).choice(N, 512, replace=False))
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G,
+                                              rows=rows)
+    check(y[:, rows], y_ref, a_ref, "4096x4096 sampled")
