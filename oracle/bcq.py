@@ -20,6 +20,8 @@ factors of Sec. 4.1 (Eq. 2, one term):
 * ``binary_search`` -- the BS step: with alpha fixed, each element takes the
   codes whose value sum_i alpha_i b_i is nearest to it (the binary search over
   the sorted 2^q representable values finds exactly this nearest value).
+* ``pot_terms`` -- Eq. 2 with several terms (additive PoT): term t is the PoT
+  of the residual alpha - sum_{j<t} a_j.
 * ``quantize`` -- greedy initialisation, then T cycles of LS, PoT, BS; the
   output is the hot-path format: planes s_i = sign(alpha_i) b_i (the sign of the
   factor folded into the plane) and int8 exponents e_i = P_i, so that
@@ -128,6 +130,25 @@ def pot_values(alpha: np.ndarray) -> np.ndarray:
     return np.where(np.abs(alpha) == 0, 0.0, sgn * np.ldexp(1.0, P))
 
 
+def pot_terms(alpha: np.ndarray, terms: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Additive PoT (Eq. 2 with ``terms`` terms): term t rounds the residual
+    of the previous terms, a_t = POT(alpha - sum_{j<t} a_j).  Returns the
+    value sum_t a_t (summed in term order from 0), and the per-term signs
+    (+-1, 0 for a zero residual) and exponents P_t, each [terms][...]."""
+    r = np.asarray(alpha, np.float64).copy()
+    val = np.zeros_like(r)
+    sgns = np.empty((terms,) + r.shape)
+    Ps = np.empty((terms,) + r.shape, dtype=np.int64)
+    for t in range(terms):
+        sg, P = pot(r)
+        a_t = pot_values(r)
+        sgns[t] = np.where(r == 0, 0.0, sg)
+        Ps[t] = P
+        val = val + a_t
+        r = r - a_t
+    return val, sgns, Ps
+
+
 def code_values(a: np.ndarray) -> np.ndarray:
     """value[s][c] = sum_i a[s][i] (bit i of c ? +1 : -1), summed in plane order."""
     S, q = a.shape
@@ -152,20 +173,29 @@ def binary_search(a: np.ndarray, w: np.ndarray) -> np.ndarray:
     return B
 
 
-def quantize_segments(w: np.ndarray, q: int, cycles: int, trace: bool = False):
-    """Alg. 1 with PoT scales on segments [S][G]; returns (B, pot alphas)."""
+def quantize_segments(w: np.ndarray, q: int, cycles: int, trace: bool = False, terms: int = 1):
+    """Alg. 1 with PoT scales (``terms`` additive terms each) on segments
+    [S][G]; returns (B, PoT alphas) -- and the per-error trace when asked."""
+    B, A, pa, errors = _alternate(w, q, cycles, terms, trace)
+    return (B, pa, errors) if trace else (B, pa)
+
+
+def _alternate(w: np.ndarray, q: int, cycles: int, terms: int, trace: bool = False):
+    """The steps of Alg. 1: (codes B, the last unrounded scales A, their PoT
+    values pa, error trace)."""
     B, A = greedy(w, q)
     errors = []
     if trace:
         errors.append(np.square(w - np.einsum("si,sig->sg", A, B)).sum(axis=1))
-    pa = pot_values(A)
+    rounded = (lambda a: pot_values(a)) if terms == 1 else (lambda a: pot_terms(a, terms)[0])
+    pa = rounded(A)
     for _ in range(cycles):
         A = least_squares(B, w)
-        pa = pot_values(A)
+        pa = rounded(A)
         B = binary_search(pa, w)
         if trace:
             errors.append(np.square(w - np.einsum("si,sig->sg", pa, B)).sum(axis=1))
-    return (B, pa, errors) if trace else (B, pa)
+    return B, A, pa, errors
 
 
 def quantize(w: np.ndarray, q: int, group: int, cycles: int):
@@ -179,6 +209,33 @@ def quantize(w: np.ndarray, q: int, group: int, cycles: int):
     signs = signs.reshape(N, NG, q, group).transpose(2, 0, 1, 3).reshape(q, N, K)
     exps = P.astype(np.int8).reshape(N, NG, q).transpose(2, 0, 1)
     return np.ascontiguousarray(signs), np.ascontiguousarray(exps)
+
+
+def quantize_terms(w: np.ndarray, q: int, group: int, cycles: int, terms: int):
+    """W [N][K] -> (signs int8 [q][N][K], exps int8 [terms][q][N][K/group],
+    term_signs int8 [terms][q][N][K/group]) with additive PoT scales: the
+    scale of (plane, row, group) is sum_t term_signs[t] 2^exps[t].  The sign of
+    the first term is folded into the plane (a zero scale keeps the plane's
+    codes and gets term sign 0), so term 0 has sign +1 or 0 and later terms
+    carry their sign relative to it."""
+    N, K = w.shape
+    NG = K // group
+    B, A, pa, _ = _alternate(segments(w, group), q, cycles, terms)
+    _, sg, P = pot_terms(A, terms)                     # [T][S][q]
+    s0 = np.where(sg[0] < 0, -1.0, 1.0)               # [S][q]
+    signs = (B * s0[:, :, None]).astype(np.int8)
+    signs = signs.reshape(N, NG, q, group).transpose(2, 0, 1, 3).reshape(q, N, K)
+    tsg = (sg * s0[None]).astype(np.int8)             # term 0 -> +1 (or 0)
+    exps = P.astype(np.int8).reshape(terms, N, NG, q).transpose(0, 3, 1, 2)
+    tsg = tsg.reshape(terms, N, NG, q).transpose(0, 3, 1, 2)
+    return np.ascontiguousarray(signs), np.ascontiguousarray(exps), np.ascontiguousarray(tsg)
+
+
+def reconstruct_terms(signs: np.ndarray, exps: np.ndarray, term_signs: np.ndarray,
+                      group: int) -> np.ndarray:
+    """W_q [N][K] = sum_i (sum_t term_signs[t] 2^exps[t]) * signs, in fp64."""
+    f = (term_signs.astype(np.float64) * np.ldexp(1.0, exps.astype(np.int64))).sum(axis=0)
+    return (np.repeat(f, group, axis=2) * signs).sum(axis=0)
 
 
 def reconstruct(signs: np.ndarray, exps: np.ndarray, group: int) -> np.ndarray:

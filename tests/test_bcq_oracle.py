@@ -14,12 +14,14 @@ than the oracle itself:
 * mutations: copies of the quantizer with one plausible mistake fail a pin.
 """
 import itertools
+from fractions import Fraction
 import json
 import os
 
 import numpy as np
 import pytest
 
+import workloads
 from oracle import bcq
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -241,3 +243,74 @@ def test_mutations_fail_pins(monkeypatch):
     vals = bcq.code_values(np.array([[2.0, 1.0]]))[0]
     dist = np.abs(-2.0 - vals)
     assert int(np.flatnonzero(dist == dist.min())[-1]) == 2
+
+
+# ----------------------------------------------------------- additive PoT (Eq. 2, several terms)
+
+def test_pot_terms_hand_example():
+    # alpha = 0.8: round(log2 0.8) = 0 -> +1; residual -0.2 -> round(log2 0.2) = -2 -> -1/4;
+    # residual 0.05 -> round(log2 0.05) = -4 -> +1/16; value 1 - 1/4 + 1/16 = 0.8125
+    v, sg, P = bcq.pot_terms(np.array([0.8]), 3)
+    assert v.tolist() == [0.8125]
+    assert sg.ravel().tolist() == [1, -1, 1] and P.ravel().tolist() == [0, -2, -4]
+
+
+def test_pot_terms_one_term_is_pot():
+    a = np.random.default_rng(1).standard_normal(1000) * 0.03
+    v, sg, P = bcq.pot_terms(a, 1)
+    s1, P1 = bcq.pot(a)
+    assert np.array_equal(v, bcq.pot_values(a)) and np.array_equal(P[0], P1)
+    assert np.array_equal(sg[0], s1)
+
+
+def test_pot_terms_residuals_are_exact_and_contract():
+    """Each term is within a factor sqrt(2) of its residual, so the subtraction
+    is exact (Sterbenz) and the residual shrinks by at least sqrt(2) - 1."""
+    a = np.random.default_rng(2).standard_normal(2000) * 0.05
+    r = a.copy()
+    for T in range(1, 5):
+        v, sg, P = bcq.pot_terms(a, T)
+        r_new = a - v
+        for x, vv in zip(a[:50], v[:50]):
+            assert Fraction(float(x)) - Fraction(float(vv)) == Fraction(float(x - vv))
+        assert (np.abs(r_new) <= (np.sqrt(2) - 1) * np.abs(r) + 1e-300).all()
+        r = r_new
+
+
+def test_pot_terms_zero_and_powers_of_two():
+    v, sg, P = bcq.pot_terms(np.array([0.0, 0.25, -4.0]), 3)
+    assert v.tolist() == [0.0, 0.25, -4.0]
+    assert sg[:, 0].tolist() == [0, 0, 0]
+    assert sg[:, 1].tolist() == [1, 0, 0] and sg[:, 2].tolist() == [-1, 0, 0]
+
+
+def test_quantize_terms_one_term_is_quantize():
+    w = workloads.fp_weights(16, 512, seed=5)
+    s1, e1 = bcq.quantize(w, 3, 128, 2)
+    s, e, t = bcq.quantize_terms(w, 3, 128, 2, 1)
+    assert np.array_equal(s, s1) and np.array_equal(e[0], e1)
+    assert set(np.unique(t)) <= {0, 1}
+
+
+def test_quantize_terms_format_and_error():
+    w = workloads.fp_weights(32, 512, seed=6)
+    errs = []
+    for T in (1, 2, 3):
+        s, e, t = bcq.quantize_terms(w, 3, 128, 2, T)
+        assert (t[0] >= 0).all() and set(np.unique(t)) <= {-1, 0, 1}
+        B, pa = bcq.quantize_segments(bcq.segments(w, 128), 3, 2, terms=T)
+        direct = np.einsum("si,sig->sg", pa, B).reshape(w.shape)
+        assert np.array_equal(bcq.reconstruct_terms(s, e, t, 128), direct)
+        errs.append(np.linalg.norm(direct - w) / np.linalg.norm(w))
+    assert errs[1] < errs[0] and errs[2] <= errs[1] * 1.01
+
+
+def test_pot_terms_mutation_without_residual_fails(monkeypatch):
+    def no_residual(alpha, terms):      # every term rounds alpha itself
+        v = np.zeros_like(alpha)
+        for _ in range(terms):
+            v = v + bcq.pot_values(alpha)
+        return v, None, None
+    monkeypatch.setattr(bcq, "pot_terms", no_residual)
+    with pytest.raises(AssertionError):
+        test_pot_terms_hand_example()
