@@ -161,6 +161,21 @@ SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const
 SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int cycles,
                            int8_t *signs, int8_t *exps, void *stream);
 
+/* The same reparameterization with additive power-of-two scales (Eq. 2 with
+ * `terms` terms): wherever a scale is rounded, term t is the power of two
+ * nearest (in the log domain) to the residual r = alpha - sum_{j<t} a_j, with
+ * the sign of r (a zero residual gives no term: sign 0, exponent -128), and
+ * BS uses the sum of the terms.  The result is the format of
+ * sa_shiftadd_gemm_terms: the sign of the first term is folded into the
+ * plane, term signs are relative to it (term 0 is +1, or 0 for a zero scale).
+ *   exps, term_signs  (device) int8 [terms][q][N][K/group], fully overwritten.
+ *   1 <= terms <= SA_MAX_TERMS (else SA_ERR_SHAPE); term_signs non-NULL;
+ *   other arguments as for sa_quantize_bcq.  With terms = 1 the planes and
+ *   exponents equal those of sa_quantize_bcq. */
+SA_API int sa_quantize_bcq_terms(const float *w, int N, int K, int q, int group, int cycles,
+                                 int terms, int8_t *signs, int8_t *exps, int8_t *term_signs,
+                                 void *stream);
+
 /* Launch geometry sa_shiftadd_gemm uses for a shape (host-only, no HIP call). */
 typedef struct {
     int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel

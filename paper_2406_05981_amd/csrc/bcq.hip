@@ -82,6 +82,51 @@ __device__ inline double pot_value(double a, int* P_out) {
     return a < 0 ? -v : v;
 }
 
+// Additive PoT (Eq. 2 with `terms` terms): term t is the PoT of the residual
+// the previous terms leave.  Returns the value (summed in term order from 0);
+// packs each term's exponent and sign (+-1, 0 for a zero residual) into byte t
+// of *pe and *ps.  One term is pot_value.
+__device__ inline double pot_terms(double a, int terms, uint32_t* pe, uint32_t* ps) {
+    double r = a, val = 0.0;
+    uint32_t e = 0, sg = 0;
+#pragma unroll
+    for (int t = 0; t < SA_MAX_TERMS; ++t) {
+        if (t < terms) {
+            int P;
+            const double v = pot_value(r, &P);
+            const int s1 = r == 0.0 ? 0 : (r < 0.0 ? -1 : 1);
+            e |= (uint32_t)(uint8_t)(int8_t)P << (8 * t);
+            sg |= (uint32_t)(uint8_t)(int8_t)s1 << (8 * t);
+            val = val + v;
+            r = r - v;
+        }
+    }
+    *pe = e;
+    *ps = sg;
+    return val;
+}
+
+// Writes the exponents (and, when tsg is given, the term signs relative to the
+// first term, whose sign goes into the plane) of one segment: plane i, term t
+// at offset t * term_stride + i * ex_plane.
+template <int Q>
+__device__ inline void write_scales(const uint32_t (&pe)[Q], const uint32_t (&ps)[Q], int terms,
+                                    int8_t* __restrict__ ex, int8_t* __restrict__ tsg,
+                                    int64_t ex_plane, int64_t term_stride) {
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+        const int s0 = (int8_t)(ps[i] & 0xffu) < 0 ? -1 : 1;
+#pragma unroll
+        for (int t = 0; t < SA_MAX_TERMS; ++t) {
+            if (t < terms) {
+                const int64_t at = t * term_stride + i * ex_plane;
+                ex[at] = (int8_t)(pe[i] >> (8 * t));
+                if (tsg) tsg[at] = (int8_t)((int)(int8_t)(ps[i] >> (8 * t)) * s0);
+            }
+        }
+    }
+}
+
 // LS step on the wave's q x q system (every lane runs it on the same values).
 template <int Q>
 __device__ void solve_ls(double (*a)[Q], double* rhs, double* alpha, double tol) {
@@ -201,8 +246,8 @@ __device__ inline bool solve_ls_regs(double (&a)[Q][Q], double (&rhs)[Q], double
 
 template <int Q>
 __global__ __launch_bounds__(kQuantThreads) void k_quantize_bcq(
-    const float* __restrict__ w, int N, int K, int G, int cycles, int8_t* __restrict__ signs,
-    int8_t* __restrict__ exps) {
+    const float* __restrict__ w, int N, int K, int G, int cycles, int terms,
+    int8_t* __restrict__ signs, int8_t* __restrict__ exps, int8_t* __restrict__ tsg) {
     __shared__ double s_val[kWaves][1 << Q];
     __shared__ double s_a[kWaves][Q][Q];
     __shared__ double s_rhs[kWaves][Q];
@@ -236,9 +281,9 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_bcq(
         alpha[i] = wave_sum_f64(part) / G;
     }
     double pa[Q];
-    int P[Q];
+    uint32_t pe[Q], ps[Q];
 #pragma unroll
-    for (int i = 0; i < Q; ++i) pa[i] = pot_value(alpha[i], &P[i]);
+    for (int i = 0; i < Q; ++i) pa[i] = pot_terms(alpha[i], terms, &pe[i], &ps[i]);
 
     for (int t = 0; t < cycles; ++t) {
         // LS: B^T w, and B^T B from the disagreements of each pair of planes
@@ -278,7 +323,7 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_bcq(
         wave_sync();
         // PoT, then the table of code values sum_i +-pa_i (in plane order)
 #pragma unroll
-        for (int i = 0; i < Q; ++i) pa[i] = pot_value(s_alpha[wv][i], &P[i]);
+        for (int i = 0; i < Q; ++i) pa[i] = pot_terms(s_alpha[wv][i], terms, &pe[i], &ps[i]);
         for (int c = lane; c < (1 << Q); c += 64) {
             double val = 0.0;
 #pragma unroll
@@ -302,20 +347,20 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_bcq(
         }
         wave_sync();  // the next cycle's table overwrites s_val
     }
-    // layer format: planes s_i = sign(pa_i) b_i, exponents P_i
+    // layer format: planes s_i = (sign of the first term of pa_i) b_i, exponents
+    // (and term signs) per term
     for (int k = lane; k < G; k += 64) {
         const uint32_t c = code[k];
 #pragma unroll
         for (int i = 0; i < Q; ++i) {
             const int b = (c >> i) & 1u ? 1 : -1;
-            cs[i * plane + k] = (int8_t)(pa[i] < 0 ? -b : b);
+            cs[i * plane + k] = (int8_t)((int8_t)(ps[i] & 0xffu) < 0 ? -b : b);
         }
     }
-    if (lane < Q) {
-        int Pi = P[0];
-#pragma unroll
-        for (int i = 1; i < Q; ++i) Pi = lane == i ? P[i] : Pi;
-        exps[((int64_t)lane * N + n) * NG + g] = (int8_t)Pi;
+    if (lane == 0) {
+        const int64_t at = (int64_t)n * NG + g;
+        write_scales<Q>(pe, ps, terms, exps + at, tsg ? tsg + at : nullptr, (int64_t)N * NG,
+                        (int64_t)Q * N * NG);
     }
 }
 
@@ -376,9 +421,9 @@ struct SegLds {
 // of 8, since G is a multiple of 8 and E is 8 or more.
 template <int Q, int E, int LN, bool FULL>
 __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int G, int cycles,
-                                        int8_t* __restrict__ cs, int64_t plane,
-                                        int8_t* __restrict__ ex, int64_t ex_plane,
-                                        SegLds<Q, LN>& lds) {
+                                        int terms, int8_t* __restrict__ cs, int64_t plane,
+                                        int8_t* __restrict__ ex, int8_t* __restrict__ tsg,
+                                        int64_t ex_plane, SegLds<Q, LN>& lds) {
     constexpr int NV = 1 << Q;
     constexpr bool kTableInLds = Q > 4;
     auto& s_a = lds.a;
@@ -412,9 +457,9 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
         m[i] = mi & vm;
     }
     double pa[Q];
-    int P[Q];
+    uint32_t pe[Q], ps[Q];
 #pragma unroll
-    for (int i = 0; i < Q; ++i) pa[i] = pot_value(alpha[i], &P[i]);
+    for (int i = 0; i < Q; ++i) pa[i] = pot_terms(alpha[i], terms, &pe[i], &ps[i]);
 
     for (int t = 0; t < cycles; ++t) {
         // LS: B^T w per plane, B^T B from popcounts of mask pairs
@@ -484,7 +529,7 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
             for (int i = 0; i < Q; ++i) al[i] = s_alpha[sb][i];
         }
 #pragma unroll
-        for (int i = 0; i < Q; ++i) pa[i] = pot_value(al[i], &P[i]);
+        for (int i = 0; i < Q; ++i) pa[i] = pot_terms(al[i], terms, &pe[i], &ps[i]);
 
         // BS against the 2^q code values sum_i +-pa_i (plane order)
         uint32_t mn[Q];
@@ -545,7 +590,7 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
     // times 0xfe, xor 0xffffffff.
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
-        const uint32_t bits = (pa[i] < 0 ? ~m[i] : m[i]);
+        const uint32_t bits = ((int8_t)(ps[i] & 0xffu) < 0 ? ~m[i] : m[i]);
         uint32_t word[E / 4 > 0 ? E / 4 : 1];
 #pragma unroll
         for (int u = 0; u < E / 4; ++u) {
@@ -566,12 +611,7 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
                     *reinterpret_cast<uint2*>(dst + 8 * u) = make_uint2(word[2 * u], word[2 * u + 1]);
         }
     }
-    if (l < Q) {
-        int Pi = P[0];
-#pragma unroll
-        for (int i = 1; i < Q; ++i) Pi = l == i ? P[i] : Pi;
-        ex[l * ex_plane] = (int8_t)Pi;
-    }
+    if (l == 0) write_scales<Q>(pe, ps, terms, ex, tsg, ex_plane, Q * ex_plane);
 }
 
 // Each group of LN lanes walks the segments with a stride of the whole grid
@@ -580,8 +620,8 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
 // most 256 VGPRs) measured faster than one wave with more registers.
 template <int Q, int E, int LN, bool FULL>
 __global__ __launch_bounds__(kQuantThreads, 2) void k_quantize_seg(
-    const float* __restrict__ w, int N, int K, int G, int cycles, int8_t* __restrict__ signs,
-    int8_t* __restrict__ exps) {
+    const float* __restrict__ w, int N, int K, int G, int cycles, int terms,
+    int8_t* __restrict__ signs, int8_t* __restrict__ exps, int8_t* __restrict__ tsg) {
     constexpr int kSegs = kQuantThreads / LN;
     __shared__ SegLds<Q, LN> lds;
     const int l = threadIdx.x & (LN - 1);
@@ -623,29 +663,34 @@ __global__ __launch_bounds__(kQuantThreads, 2) void k_quantize_seg(
         for (int e = 0; e < E; ++e) wf[e] = wn[e];
         if (seg + stride < total) load(seg + stride, wn);
         const int n = (int)(seg / NG), g = (int)(seg % NG);
-        quantize_segment<Q, E, LN, FULL>(wf, l, sb, G, cycles,
+        const int64_t at = (int64_t)n * NG + g;
+        quantize_segment<Q, E, LN, FULL>(wf, l, sb, G, cycles, terms,
                                          signs + (int64_t)n * K + (int64_t)g * G, plane,
-                                         exps + (int64_t)n * NG + g, ex_plane, lds);
+                                         exps + at, tsg ? tsg + at : nullptr, ex_plane, lds);
     }
 }
 
+struct QuantArgs {
+    const float* w;
+    int N, K, G, cycles, terms;
+    int8_t* signs;
+    int8_t* exps;
+    int8_t* tsg;
+    int64_t segs;
+};
+
 template <int Q, int E, int LN>
-void launch_seg(const float* w, int N, int K, int G, int cycles, int8_t* signs, int8_t* exps,
-                int64_t segs, hipStream_t s) {
+void launch_seg(const QuantArgs& a, hipStream_t s) {
     constexpr int kSegs = kQuantThreads / LN;
-    const int64_t blocks = (segs + kSegs - 1) / kSegs;
+    const int64_t blocks = (a.segs + kSegs - 1) / kSegs;
     const unsigned grid = (unsigned)(blocks < kSegMaxBlocks ? blocks : kSegMaxBlocks);
-    if constexpr (E < 8) {  // only ever full (G = 8 or 16)
+    const bool full = E < 8 || a.G == LN * E;  // E < 8: only ever full (G = 8 or 16)
+    if (full)
         hipLaunchKernelGGL((k_quantize_seg<Q, E, LN, true>), dim3(grid), dim3(kQuantThreads), 0,
-                           s, w, N, K, G, cycles, signs, exps);
-    } else {
-        if (G == LN * E)
-            hipLaunchKernelGGL((k_quantize_seg<Q, E, LN, true>), dim3(grid), dim3(kQuantThreads),
-                               0, s, w, N, K, G, cycles, signs, exps);
-        else
-            hipLaunchKernelGGL((k_quantize_seg<Q, E, LN, false>), dim3(grid), dim3(kQuantThreads),
-                               0, s, w, N, K, G, cycles, signs, exps);
-    }
+                           s, a.w, a.N, a.K, a.G, a.cycles, a.terms, a.signs, a.exps, a.tsg);
+    else if constexpr (E >= 8)
+        hipLaunchKernelGGL((k_quantize_seg<Q, E, LN, false>), dim3(grid), dim3(kQuantThreads), 0,
+                           s, a.w, a.N, a.K, a.G, a.cycles, a.terms, a.signs, a.exps, a.tsg);
 }
 
 // Lanes per segment and slots per lane.  q <= 4: 4 lanes up to G = 128 (E =
@@ -653,37 +698,42 @@ void launch_seg(const float* w, int N, int K, int G, int cycles, int8_t* signs, 
 // empty), 8 lanes of 32 slots above.  q > 4 (the 2^q code values in LDS): 16
 // lanes of 16 slots, 16 segments per workgroup.
 template <int Q>
-void launch_seg_e(const float* w, int N, int K, int G, int cycles, int8_t* signs, int8_t* exps,
-                  int64_t segs, hipStream_t s) {
+void launch_seg_e(const QuantArgs& a, hipStream_t s) {
     if constexpr (Q > 4) {
-        launch_seg<Q, 16, 16>(w, N, K, G, cycles, signs, exps, segs, s);
+        launch_seg<Q, 16, 16>(a, s);
     } else {
-        if (G == 8)
-            launch_seg<Q, 2, 4>(w, N, K, G, cycles, signs, exps, segs, s);
-        else if (G == 16)
-            launch_seg<Q, 4, 4>(w, N, K, G, cycles, signs, exps, segs, s);
-        else if (G <= 32)
-            launch_seg<Q, 8, 4>(w, N, K, G, cycles, signs, exps, segs, s);
-        else if (G <= 64)
-            launch_seg<Q, 16, 4>(w, N, K, G, cycles, signs, exps, segs, s);
-        else if (G <= 128)
-            launch_seg<Q, 32, 4>(w, N, K, G, cycles, signs, exps, segs, s);
+        if (a.G == 8)
+            launch_seg<Q, 2, 4>(a, s);
+        else if (a.G == 16)
+            launch_seg<Q, 4, 4>(a, s);
+        else if (a.G <= 32)
+            launch_seg<Q, 8, 4>(a, s);
+        else if (a.G <= 64)
+            launch_seg<Q, 16, 4>(a, s);
+        else if (a.G <= 128)
+            launch_seg<Q, 32, 4>(a, s);
         else
-            launch_seg<Q, 32, 8>(w, N, K, G, cycles, signs, exps, segs, s);
+            launch_seg<Q, 32, 8>(a, s);
     }
 }
 
 template <int Q>
-void launch(const float* w, int N, int K, int G, int cycles, int8_t* signs, int8_t* exps,
-            unsigned grid, hipStream_t s) {
-    hipLaunchKernelGGL(k_quantize_bcq<Q>, dim3(grid), dim3(kQuantThreads), 0, s, w, N, K, G,
-                       cycles, signs, exps);
+void launch_wave(const QuantArgs& a, hipStream_t s) {
+    const unsigned grid = (unsigned)((a.segs + kWaves - 1) / kWaves);
+    hipLaunchKernelGGL(k_quantize_bcq<Q>, dim3(grid), dim3(kQuantThreads), 0, s, a.w, a.N, a.K,
+                       a.G, a.cycles, a.terms, a.signs, a.exps, a.tsg);
 }
 
-}  // namespace
+template <int Q>
+void launch_q(const QuantArgs& a, hipStream_t s) {
+    if (a.G <= kSegMaxGroup)
+        launch_seg_e<Q>(a, s);
+    else
+        launch_wave<Q>(a, s);
+}
 
-SA_API int sa_quantize_bcq(const float* w, int N, int K, int q, int group, int cycles,
-                           int8_t* signs, int8_t* exps, void* stream) {
+int quantize(const float* w, int N, int K, int q, int group, int cycles, int terms,
+             int8_t* signs, int8_t* exps, int8_t* tsg, void* stream) {
     if (!w || !signs || !exps) return SA_ERR_NULL;
     if (q < 1 || q > SA_MAX_Q) return SA_ERR_Q;
     if (N < 1 || K < 8 || (K & 7)) return SA_ERR_SHAPE;
@@ -691,35 +741,35 @@ SA_API int sa_quantize_bcq(const float* w, int N, int K, int q, int group, int c
     if ((int64_t)N * (K / 8) >= (int64_t)1 << 31) return SA_ERR_SHAPE;
     if (group < 8 || (group & 7) || (K % group)) return SA_ERR_GROUP;
     if (cycles < 0 || cycles > SA_MAX_CYCLES) return SA_ERR_SHAPE;
+    if (terms < 1 || terms > SA_MAX_TERMS) return SA_ERR_SHAPE;
     if ((reinterpret_cast<uintptr_t>(w) & 15u) || (reinterpret_cast<uintptr_t>(signs) & 7u))
         return SA_ERR_ALIGN;
-    const int64_t segs = (int64_t)N * (K / group);
-    const int64_t grid = (segs + kWaves - 1) / kWaves;
-    if (grid > 0x7fffffff) return SA_ERR_SHAPE;
+    QuantArgs a{w, N, K, group, cycles, terms, signs, exps, tsg, (int64_t)N * (K / group)};
+    if ((a.segs + kWaves - 1) / kWaves > 0x7fffffff) return SA_ERR_SHAPE;
     const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const unsigned gd = (unsigned)grid;
-    if (group <= kSegMaxGroup) {
-        switch (q) {
-            case 1: launch_seg_e<1>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 2: launch_seg_e<2>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 3: launch_seg_e<3>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 4: launch_seg_e<4>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 5: launch_seg_e<5>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 6: launch_seg_e<6>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            case 7: launch_seg_e<7>(w, N, K, group, cycles, signs, exps, segs, s); break;
-            default: launch_seg_e<8>(w, N, K, group, cycles, signs, exps, segs, s); break;
-        }
-        return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP;
-    }
     switch (q) {
-        case 1: launch<1>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 2: launch<2>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 3: launch<3>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 4: launch<4>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 5: launch<5>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 6: launch<6>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        case 7: launch<7>(w, N, K, group, cycles, signs, exps, gd, s); break;
-        default: launch<8>(w, N, K, group, cycles, signs, exps, gd, s); break;
+        case 1: launch_q<1>(a, s); break;
+        case 2: launch_q<2>(a, s); break;
+        case 3: launch_q<3>(a, s); break;
+        case 4: launch_q<4>(a, s); break;
+        case 5: launch_q<5>(a, s); break;
+        case 6: launch_q<6>(a, s); break;
+        case 7: launch_q<7>(a, s); break;
+        default: launch_q<8>(a, s); break;
     }
     return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+}  // namespace
+
+SA_API int sa_quantize_bcq(const float* w, int N, int K, int q, int group, int cycles,
+                           int8_t* signs, int8_t* exps, void* stream) {
+    return quantize(w, N, K, q, group, cycles, 1, signs, exps, nullptr, stream);
+}
+
+SA_API int sa_quantize_bcq_terms(const float* w, int N, int K, int q, int group, int cycles,
+                                 int terms, int8_t* signs, int8_t* exps, int8_t* term_signs,
+                                 void* stream) {
+    if (!term_signs) return SA_ERR_NULL;
+    return quantize(w, N, K, q, group, cycles, terms, signs, exps, term_signs, stream);
 }

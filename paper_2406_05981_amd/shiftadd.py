@@ -52,6 +52,7 @@ def _bind(lib):
         "sa_shiftadd_gemm_terms": ([P, P, P, P, I, I, I, I, I, I, P, P], I),
         "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
         "sa_quantize_bcq": ([P, I, I, I, I, I, P, P, P], I),
+        "sa_quantize_bcq_terms": ([P, I, I, I, I, I, I, P, P, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
         "sa_version": ([], ctypes.c_char_p),
     }
@@ -237,6 +238,21 @@ def sa_quantize_bcq(w: torch.Tensor, N: int, K: int, q: int, group: int, cycles:
         "sa_quantize_bcq")
 
 
+def sa_quantize_bcq_terms(w: torch.Tensor, N: int, K: int, q: int, group: int, cycles: int,
+                          terms: int, signs: torch.Tensor, exps: torch.Tensor,
+                          term_signs: torch.Tensor, stream=None) -> None:
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_quantize_bcq_terms")
+    if terms < 1 or terms > SA_MAX_TERMS:
+        _check(SA_ERR_SHAPE, "sa_quantize_bcq_terms")
+    n_e = terms * q * N * (K // group)
+    _check(lib.sa_quantize_bcq_terms(
+        _dev(w, "w", torch.float32, N * K), N, K, q, group, cycles, terms,
+        _dev(signs, "signs", torch.int8, q * N * K),
+        _dev(exps, "exps", torch.int8, n_e), _dev(term_signs, "term_signs", torch.int8, n_e),
+        _stream(stream)), "sa_quantize_bcq_terms")
+
+
 def sa_read_probe(buf: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None) -> None:
     """Plain read of ``nbytes`` bytes of ``buf`` (a measurement aid, see the header)."""
     if not isinstance(buf, torch.Tensor) or not buf.is_cuda:
@@ -258,6 +274,18 @@ def quantize_bcq(w: torch.Tensor, q: int, group: int, cycles: int, stream=None):
     exps = torch.empty((q, N, K // group), dtype=torch.int8, device=w.device)
     sa_quantize_bcq(w, N, K, q, group, cycles, signs, exps, stream)
     return signs, exps
+
+
+def quantize_bcq_terms(w: torch.Tensor, q: int, group: int, cycles: int, terms: int,
+                       stream=None):
+    """``(signs [q][N][K], exps [terms][q][N][K/group], term_signs [terms][q][N][K/group])``
+    (int8, new device tensors) with additive PoT scales."""
+    N, K = w.shape
+    signs = torch.empty((q, N, K), dtype=torch.int8, device=w.device)
+    exps = torch.empty((terms, q, N, K // group), dtype=torch.int8, device=w.device)
+    tsg = torch.empty((terms, q, N, K // group), dtype=torch.int8, device=w.device)
+    sa_quantize_bcq_terms(w, N, K, q, group, cycles, terms, signs, exps, tsg, stream)
+    return signs, exps, tsg
 
 
 def pack_weights(signs: torch.Tensor, stream=None) -> torch.Tensor:

@@ -239,3 +239,18 @@ def test_terms_validation_codes():
     assert call(T=0) == sa.SA_ERR_SHAPE
     assert call(T=sa.SA_MAX_TERMS + 1) == sa.SA_ERR_SHAPE
     assert call(x=A + 8) == sa.SA_ERR_ALIGN
+
+
+def test_quantize_terms_validation_codes():
+    f = sa.lib.sa_quantize_bcq_terms
+
+    def call(w=A, N=16, K=256, q=3, G=128, T=2, n=2, s=A, e=A, t=A):
+        return f(w, N, K, q, G, T, n, s, e, t, None)
+
+    assert call(t=None) == sa.SA_ERR_NULL
+    assert call(w=None) == sa.SA_ERR_NULL
+    assert call(n=0) == sa.SA_ERR_SHAPE
+    assert call(n=sa.SA_MAX_TERMS + 1) == sa.SA_ERR_SHAPE
+    assert call(q=9) == sa.SA_ERR_Q
+    assert call(G=96) == sa.SA_ERR_GROUP
+    assert call(w=A + 8) == sa.SA_ERR_ALIGN

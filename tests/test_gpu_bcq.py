@@ -227,3 +227,64 @@ def test_quantize_then_layer():
     assert (np.abs(y - y_ref) / a_ref).max() <= 2e-3
     y_dense = x.astype(np.float64) @ bcq.reconstruct(s, e, G).T
     assert np.abs(y_ref - y_dense).max() <= 1e-12 * a_ref.max()
+
+
+# ------------------------------------------------------------ additive PoT scales
+
+def gpu_quantize_terms(w, q, G, T, terms):
+    s, e, t = sa.quantize_bcq_terms(torch.from_numpy(np.ascontiguousarray(w)).cuda(), q, G, T,
+                                    terms)
+    torch.cuda.synchronize()
+    return s.cpu().numpy(), e.cpu().numpy(), t.cpu().numpy()
+
+
+TERM_SHAPES = [
+    # (q, N, K, G, T, terms, label)
+    (3, 130, 512, 128, 2, 1, "one term: the single-term format"),
+    (3, 130, 512, 128, 2, 2, "two terms"),
+    (2, 64, 1024, 256, 3, 3, "three terms, G = 256"),
+    (4, 40, 384, 64, 0, 4, "four terms, greedy scales only"),
+    (6, 9, 1024, 512, 2, 2, "q = 6, wave per segment"),
+    (3, 5, 4096, 4096, 1, 3, "G = K"),
+]
+
+
+@pytest.mark.parametrize("q,N,K,G,T,terms,label", TERM_SHAPES, ids=[c[-1] for c in TERM_SHAPES])
+def test_quantize_terms_parity(q, N, K, G, T, terms, label):
+    say(f"[bcq terms] {label}: N={N} K={K} q={q} G={G} T={T} terms={terms}")
+    w = workloads.fp_weights(N, K, seed=q * 13 + terms)
+    s, e, t = gpu_quantize_terms(w, q, G, T, terms)
+    s_ref, e_ref, t_ref = bcq.quantize_terms(w, q, G, T, terms)
+    NG = K // G
+    bad = ((s != s_ref).reshape(q, N, NG, G).any(axis=(0, 3)) |
+           (e != e_ref).any(axis=(0, 1)) | (t != t_ref).any(axis=(0, 1)))
+    assert not bad.any(), f"{label}: {int(bad.sum())} segments differ"
+    if terms == 1:
+        s1, e1 = gpu_quantize(w, q, G, T)
+        assert np.array_equal(s, s1) and np.array_equal(e[0], e1)
+
+
+def test_quantize_terms_then_layer():
+    """Additive scales end to end: quantize with two terms, pack, run the
+    additive layer; agrees with the oracle's additive layer on the same planes
+    and with the dense product of the reconstructed weights."""
+    import oracle
+
+    N, K, q, G, T, terms = 512, 1024, 3, 128, 2, 2
+    w = workloads.fp_weights(N, K, seed=22)
+    s_d, e_d, t_d = sa.quantize_bcq_terms(torch.from_numpy(w).cuda(), q, G, T, terms)
+    x = np.random.default_rng(2).standard_normal((2, K)).astype(np.float16)
+    y = torch.empty((2, N), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm_terms(torch.from_numpy(x).cuda(), sa.pack_weights(s_d), e_d, t_d, q, N, K,
+                              G, terms, 2, y)
+    torch.cuda.synchronize()
+    s, e, t = s_d.cpu().numpy(), e_d.cpu().numpy(), t_d.cpu().numpy()
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(x, s, e, t, G)
+    assert (np.abs(y.cpu().numpy() - y_ref) / a_ref).max() <= 2e-3
+    y_dense = x.astype(np.float64) @ bcq.reconstruct_terms(s, e, t, G).T
+    assert np.abs(y_ref - y_dense).max() <= 1e-12 * a_ref.max()
+    # the second term lowers the weight error
+    s1, e1 = gpu_quantize(w, q, G, T)
+    err1 = np.linalg.norm(bcq.reconstruct(s1, e1, G) - w)
+    err2 = np.linalg.norm(bcq.reconstruct_terms(s, e, t, G) - w)
+    assert err2 < err1
