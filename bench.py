@@ -52,7 +52,7 @@ def source_hash() -> str:
 
 
 KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col",
-           4: "k_gemm_rows_blk"}
+           4: "k_gemm_rows_blk", 5: "k_gemm_rows_add"}
 
 
 def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
@@ -82,6 +82,9 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
     probe_rows = np.arange(min(N, 256))
     t0 = time.perf_counter()
     def layer(rows):
+        if "term_signs" in d:
+            return oracle.shiftadd_gemm_terms(d["x"], d["signs"], d["exps"], d["term_signs"],
+                                              d["G"], nthreads=threads, rows=rows)
         if "blk_exps" in d:
             return oracle.shiftadd_gemm_blockwise(d["x"], d["signs"], d["blk_exps"],
                                                   d["row_block"], nthreads=threads, rows=rows)
@@ -331,6 +334,9 @@ def main() -> int:
     ap.add_argument("--blockwise", action="store_true",
                     help="the layer with block-wise factors (sa_shiftadd_gemm_blockwise, blocks "
                          "of 8 columns x N/8 rows) on the workload layer's shape")
+    ap.add_argument("--terms", type=int, default=0,
+                    help="the layer with additive power-of-two factors of this many terms "
+                         "(sa_shiftadd_gemm_terms) on the workload layer's shape")
     ap.add_argument("--quantize", action="store_true",
                     help="time the offline reparameterization (sa_quantize_bcq) instead")
     ap.add_argument("--shape", type=int, nargs=2, default=(4096, 4096), metavar=("N", "K"),
@@ -378,10 +384,15 @@ def main() -> int:
     L = w.layers[args.layer]
     B = args.batch or w.batches[0]
     q, N, K, G = L.q, L.N, L.K, w.group
-    colwise, blockwise = args.colwise, args.blockwise
+    colwise, blockwise, terms = args.colwise, args.blockwise, args.terms
     rb = (N + 7) // 8  # block-wise: the paper's blocks of N/8 rows
     nb = (N + rb - 1) // rb
-    if blockwise:
+    if terms:
+        # T exponent bytes and T term-sign bytes per (plane, row, group)
+        bytes_step = algorithmic_bytes(q, N, K, G, B) + (2 * terms - 1) * q * N * (K // G)
+        weight_bytes = q * N * K // 8 + 2 * terms * q * N * (K // G)
+        plan = dict(sa.sa_plan_gemm(q, N, K, G, 1), path=5)
+    elif blockwise:
         bytes_step = algorithmic_bytes(q, N, K, K, B) - q * N + q * nb * (K // 8)
         weight_bytes = q * N * K // 8 + q * nb * (K // 8)
         plan = sa.sa_plan_gemm_blockwise(q, N, K, rb, B)
@@ -395,16 +406,23 @@ def main() -> int:
         weight_bytes = q * N * K // 8 + q * N * (K // G)
         plan = sa.sa_plan_gemm(q, N, K, G, B)
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / weight_bytes))
-    mode = " column-wise" if colwise else (" block-wise" if blockwise else "")
+    mode = (" column-wise" if colwise else " block-wise" if blockwise else
+            f" additive, {terms} terms" if terms else "")
     log(f"workload {args.workload}/{L.name}{mode}: q={q} N={N} "
         f"K={K} G={G} B={B}; {copies} weight copies ({copies * weight_bytes / 1e6:.0f} MB); "
         f"plan {plan}")
 
     t0 = time.perf_counter()
-    packed, exps = [], []
+    packed, exps, tsgs = [], [], []
     d0 = None
     for c in range(copies):
-        if blockwise:
+        if terms:
+            d = workloads.terms_case(q, N, K, G, B, terms, seed=0, exp_range=w.exp_range,
+                                     outlier_fraction=w.outlier_fraction,
+                                     outlier_scale=w.outlier_scale, copy=c)
+            e = d["exps"]
+            tsgs.append(torch.from_numpy(d["term_signs"]).cuda())
+        elif blockwise:
             d = workloads.blockwise_case(q, N, K, B, rb, seed=0, exp_range=w.exp_range,
                                          outlier_fraction=w.outlier_fraction,
                                          outlier_scale=w.outlier_scale, copy=c)
@@ -434,7 +452,9 @@ def main() -> int:
 
     def step(i: int) -> None:
         c = i % copies
-        if blockwise:
+        if terms:
+            sa.sa_shiftadd_gemm_terms(x, packed[c], exps[c], tsgs[c], q, N, K, G, terms, B, y)
+        elif blockwise:
             sa.sa_shiftadd_gemm_blockwise(x, packed[c], exps[c], q, N, K, rb, B, y)
         elif colwise:
             sa.sa_shiftadd_gemm_colwise(x, packed[c], exps[c], q, N, K, B, y)
@@ -492,7 +512,8 @@ def main() -> int:
         log(f"read floor: {read_floor}")
 
     kernel = KERNELS[plan["path"]]
-    traffic = measured_traffic(kernel, args.workload, args.layer, B)
+    traffic = measured_traffic(kernel + (f"_t{terms}" if terms else ""), args.workload,
+                               args.layer, B)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -513,6 +534,7 @@ def main() -> int:
             "N": N, "K": K, "q": q, "group": None if colwise or blockwise else G, "batch": B,
             "scales": ("column-wise (one exponent per plane and column)" if colwise else
                        f"block-wise (8 columns x {rb} rows)" if blockwise else
+                       f"row-wise, group {G}, additive, {terms} terms" if terms else
                        f"row-wise, group {G}"),
             "weight_copies": copies,
             "launch": "eager" if args.eager else "hip graph replay",

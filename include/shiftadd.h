@@ -168,7 +168,7 @@ SA_API int sa_quantize_bcq(const float *w, int N, int K, int q, int group, int c
  * BS uses the sum of the terms.  The result is the format of
  * sa_shiftadd_gemm_terms: the sign of the first term is folded into the
  * plane, term signs are relative to it (term 0 is +1, or 0 for a zero scale).
- *   exps, term_signs  (device) int8 [terms][q][N][K/group], fully overwritten.
+ *   exps, term_signs  (device) int8 [q][N][K/group][terms], fully overwritten.
  *   1 <= terms <= SA_MAX_TERMS (else SA_ERR_SHAPE); term_signs non-NULL;
  *   other arguments as for sa_quantize_bcq.  With terms = 1 the planes and
  *   exponents equal those of sa_quantize_bcq. */
@@ -235,14 +235,16 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t *x, const uint8_t *packed_b
 
 /* The layer with additive power-of-two factors (Eq. 2 with T terms): the
  * factor of (plane i, row n, group g) is the greedy sum of T signed powers of
- * two, sum_t term_signs[t] 2^exps[t] (a term sign of 0 means no term):
+ * two, sum_t term_signs[..][t] 2^exps[..][t] (a term sign of 0 means no term):
  *
- *   y[b][n] = sum_i sum_g ( sum_t term_signs[t][i][n][g] 2^exps[t][i][n][g] )
+ *   y[b][n] = sum_i sum_g ( sum_t term_signs[i][n][g][t] 2^exps[i][n][g][t] )
  *                         * sum_{k in g} s_i[n][k] x[b][k]
  *
  * Each group sum is shifted once per term and added with its sign.  T = 1
  * with term sign +1 is sa_shiftadd_gemm.
- *   exps, term_signs (device) int8 [T][q][N][K/group], term signs in {-1, 0, 1}.
+ *   exps, term_signs (device) int8 [q][N][K/group][T] (the T terms of a group
+ *          are consecutive bytes; 2-byte aligned for T = 2, 4-byte for T = 4),
+ *          term signs in {-1, 0, 1}.
  *   group % 128 == 0 (else SA_ERR_GROUP); 1 <= terms <= SA_MAX_TERMS (else
  *   SA_ERR_SHAPE); other arguments and errors as for sa_shiftadd_gemm.
  * Asynchronous on `stream`; allocates nothing; deterministic. */

@@ -242,7 +242,7 @@ def shiftadd_gemm_terms(x: np.ndarray, signs: np.ndarray, exps: np.ndarray,
                         term_signs: np.ndarray, G: int, nthreads: int = 0,
                         rows: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
     """``(y, absterm)`` of the layer with additive power-of-two factors:
-    ``exps, term_signs int8 [T][q][N][K/G]``,
+    ``exps, term_signs int8 [q][N][K/G][T]``,
     ``y[b][n] = sum_i sum_g sum_t sg_t ldexp(sum_{k in g} s_i[n][k] x[b][k], e_t)``."""
     x64 = np.ascontiguousarray(np.asarray(x).astype(np.float64))
     signs = np.ascontiguousarray(signs, dtype=np.int8)
@@ -250,10 +250,10 @@ def shiftadd_gemm_terms(x: np.ndarray, signs: np.ndarray, exps: np.ndarray,
     term_signs = np.ascontiguousarray(term_signs, dtype=np.int8)
     q, N, K = signs.shape
     B = x64.shape[0]
-    T = exps.shape[0]
-    if K % 8 or G % 8 or K % G or exps.shape != (T, q, N, K // G) or term_signs.shape != exps.shape:
+    T = exps.shape[-1]
+    if K % 8 or G % 8 or K % G or exps.shape != (q, N, K // G, T) or term_signs.shape != exps.shape:
         raise ValueError(f"exps/term_signs shape {exps.shape}/{term_signs.shape} != "
-                         f"{(T, q, N, K // G)}")
+                         f"{(q, N, K // G, T)}")
     if x64.shape != (B, K):
         raise ValueError(f"x shape {x64.shape} != {(B, K)}")
     lib = _load()

@@ -212,9 +212,9 @@ def quantize(w: np.ndarray, q: int, group: int, cycles: int):
 
 
 def quantize_terms(w: np.ndarray, q: int, group: int, cycles: int, terms: int):
-    """W [N][K] -> (signs int8 [q][N][K], exps int8 [terms][q][N][K/group],
-    term_signs int8 [terms][q][N][K/group]) with additive PoT scales: the
-    scale of (plane, row, group) is sum_t term_signs[t] 2^exps[t].  The sign of
+    """W [N][K] -> (signs int8 [q][N][K], exps int8 [q][N][K/group][terms],
+    term_signs int8 [q][N][K/group][terms]) with additive PoT scales: the
+    scale of (plane, row, group) is sum_t term_signs[..., t] 2^exps[..., t].  The sign of
     the first term is folded into the plane (a zero scale keeps the plane's
     codes and gets term sign 0), so term 0 has sign +1 or 0 and later terms
     carry their sign relative to it."""
@@ -226,15 +226,15 @@ def quantize_terms(w: np.ndarray, q: int, group: int, cycles: int, terms: int):
     signs = (B * s0[:, :, None]).astype(np.int8)
     signs = signs.reshape(N, NG, q, group).transpose(2, 0, 1, 3).reshape(q, N, K)
     tsg = (sg * s0[None]).astype(np.int8)             # term 0 -> +1 (or 0)
-    exps = P.astype(np.int8).reshape(terms, N, NG, q).transpose(0, 3, 1, 2)
-    tsg = tsg.reshape(terms, N, NG, q).transpose(0, 3, 1, 2)
+    exps = P.astype(np.int8).reshape(terms, N, NG, q).transpose(3, 1, 2, 0)
+    tsg = tsg.reshape(terms, N, NG, q).transpose(3, 1, 2, 0)
     return np.ascontiguousarray(signs), np.ascontiguousarray(exps), np.ascontiguousarray(tsg)
 
 
 def reconstruct_terms(signs: np.ndarray, exps: np.ndarray, term_signs: np.ndarray,
                       group: int) -> np.ndarray:
-    """W_q [N][K] = sum_i (sum_t term_signs[t] 2^exps[t]) * signs, in fp64."""
-    f = (term_signs.astype(np.float64) * np.ldexp(1.0, exps.astype(np.int64))).sum(axis=0)
+    """W_q [N][K] = sum_i (sum_t term_signs[..., t] 2^exps[..., t]) * signs, in fp64."""
+    f = (term_signs.astype(np.float64) * np.ldexp(1.0, exps.astype(np.int64))).sum(axis=-1)
     return (np.repeat(f, group, axis=2) * signs).sum(axis=0)
 
 

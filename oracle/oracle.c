@@ -265,7 +265,7 @@ void oracle_shiftadd_gemm_blockwise(const double *x, const int8_t *signs, const 
 
 /*
  * The layer with additive power-of-two factors (Eq. 2 with T terms): the
- * factor of (plane i, row n, group g) is sum_t sg[t][i][n][g] 2^e[t][i][n][g]
+ * factor of (plane i, row n, group g) is sum_t sg[i][n][g][t] 2^e[i][n][g][t]
  * with term signs in {-1, 0, +1} (0: no term), so that
  *   y       = sum_i sum_g sum_t sg_t ldexp( sum_{k in g} s_i[n][k] x[b][k], e_t )
  *   absterm = sum_i sum_g sum_t |sg_t| ldexp( sum_{k in g} |x[b][k]|, e_t )
@@ -275,7 +275,7 @@ static void one_output_terms(const double *xb, const int8_t *signs, const int8_t
                              const int8_t *term_signs, int64_t T, int64_t q, int64_t N,
                              int64_t K, int64_t G, int64_t n, double *y, double *absterm)
 {
-    const int64_t NG = K / G, plane = q * N * NG;
+    const int64_t NG = K / G;
     double total = 0.0, abs_total = 0.0;
     for (int64_t i = 0; i < q; ++i) {
         const int8_t *s = signs + (i * N + n) * K;
@@ -285,12 +285,12 @@ static void one_output_terms(const double *xb, const int8_t *signs, const int8_t
                 part += (double)s[k] * xb[k];
                 apart += fabs(xb[k]);
             }
-            const int64_t at = (i * N + n) * NG + g;
+            const int64_t at = ((i * N + n) * NG + g) * T;
             for (int64_t t = 0; t < T; ++t) {
-                const int sg = term_signs[t * plane + at];
+                const int sg = term_signs[at + t];
                 if (sg == 0) continue;
-                total += (double)sg * ldexp(part, exps[t * plane + at]);
-                abs_total += ldexp(apart, exps[t * plane + at]);
+                total += (double)sg * ldexp(part, exps[at + t]);
+                abs_total += ldexp(apart, exps[at + t]);
             }
         }
     }
@@ -298,7 +298,7 @@ static void one_output_terms(const double *xb, const int8_t *signs, const int8_t
     *absterm = abs_total;
 }
 
-/* exps, term_signs: int8 [T][q][N][K/G]; other arguments as
+/* exps, term_signs: int8 [q][N][K/G][T]; other arguments as
  * oracle_shiftadd_gemm_blockwise. */
 void oracle_shiftadd_gemm_terms(const double *x, const int8_t *signs, const int8_t *exps,
                                 const int8_t *term_signs, int64_t T, int64_t q, int64_t N,

@@ -108,18 +108,18 @@ __device__ inline double pot_terms(double a, int terms, uint32_t* pe, uint32_t* 
 
 // Writes the exponents (and, when tsg is given, the term signs relative to the
 // first term, whose sign goes into the plane) of one segment: plane i, term t
-// at offset t * term_stride + i * ex_plane.
+// at offset i * ex_plane * terms + t (the terms of a segment are consecutive).
 template <int Q>
 __device__ inline void write_scales(const uint32_t (&pe)[Q], const uint32_t (&ps)[Q], int terms,
                                     int8_t* __restrict__ ex, int8_t* __restrict__ tsg,
-                                    int64_t ex_plane, int64_t term_stride) {
+                                    int64_t ex_plane) {
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
         const int s0 = (int8_t)(ps[i] & 0xffu) < 0 ? -1 : 1;
 #pragma unroll
         for (int t = 0; t < SA_MAX_TERMS; ++t) {
             if (t < terms) {
-                const int64_t at = t * term_stride + i * ex_plane;
+                const int64_t at = i * ex_plane * terms + t;
                 ex[at] = (int8_t)(pe[i] >> (8 * t));
                 if (tsg) tsg[at] = (int8_t)((int)(int8_t)(ps[i] >> (8 * t)) * s0);
             }
@@ -358,9 +358,8 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_bcq(
         }
     }
     if (lane == 0) {
-        const int64_t at = (int64_t)n * NG + g;
-        write_scales<Q>(pe, ps, terms, exps + at, tsg ? tsg + at : nullptr, (int64_t)N * NG,
-                        (int64_t)Q * N * NG);
+        const int64_t at = ((int64_t)n * NG + g) * terms;
+        write_scales<Q>(pe, ps, terms, exps + at, tsg ? tsg + at : nullptr, (int64_t)N * NG);
     }
 }
 
@@ -611,7 +610,7 @@ __device__ inline void quantize_segment(const float (&wf)[E], int l, int sb, int
                     *reinterpret_cast<uint2*>(dst + 8 * u) = make_uint2(word[2 * u], word[2 * u + 1]);
         }
     }
-    if (l == 0) write_scales<Q>(pe, ps, terms, ex, tsg, ex_plane, Q * ex_plane);
+    if (l == 0) write_scales<Q>(pe, ps, terms, ex, tsg, ex_plane);
 }
 
 // Each group of LN lanes walks the segments with a stride of the whole grid
@@ -663,7 +662,7 @@ __global__ __launch_bounds__(kQuantThreads, 2) void k_quantize_seg(
         for (int e = 0; e < E; ++e) wf[e] = wn[e];
         if (seg + stride < total) load(seg + stride, wn);
         const int n = (int)(seg / NG), g = (int)(seg % NG);
-        const int64_t at = (int64_t)n * NG + g;
+        const int64_t at = ((int64_t)n * NG + g) * terms;
         quantize_segment<Q, E, LN, FULL>(wf, l, sb, G, cycles, terms,
                                          signs + (int64_t)n * K + (int64_t)g * G, plane,
                                          exps + at, tsg ? tsg + at : nullptr, ex_plane, lds);

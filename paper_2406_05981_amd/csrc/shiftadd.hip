@@ -246,7 +246,7 @@ struct RowsArgs {
     float* y;           // [B][N]
     int groups;         // 16-row groups of N, spread over the grid
     int row_block, NB;  // block-wise: rows per block, blocks
-    const int8_t* term_signs;  // additive: [T][q][N][K/G], with exps [T][q][N][K/G]
+    const int8_t* term_signs;  // additive: [q][N][K/G][T], with exps [q][N][K/G][T]
     int terms;                 // additive: T
 };
 
@@ -312,25 +312,25 @@ __device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, int
         j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)(plane0 + i) * a.N * C + off);
 }
 
-// Additive: the T exponents and term signs of the lane's group in every plane.
+// Additive: the T exponents and term signs of the lane's group in every plane,
+// T consecutive bytes each (one load of 1, 2 or 4 bytes; three bytes for T = 3).
+__device__ inline uint32_t load_terms(const int8_t* p, int T) {
+    const uint8_t* b = reinterpret_cast<const uint8_t*>(p);
+    if (T == 4) return *reinterpret_cast<const uint32_t*>(b);
+    if (T == 2) return *reinterpret_cast<const uint16_t*>(b);
+    if (T == 3) return (uint32_t)b[0] | ((uint32_t)b[1] << 8) | ((uint32_t)b[2] << 16);
+    return b[0];
+}
+
 template <int Q>
 __device__ inline void load_job_terms(const RowsArgs& a, int n, int J, int NG, int bpg,
                                       JobRegs<Q>& j) {
-    const uint32_t off = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg));
-    const size_t term_stride = (size_t)a.q * a.N * NG;
+    const uint32_t off = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg)) * (uint32_t)a.terms;
+    const size_t plane = (size_t)a.N * NG * a.terms;
 #pragma unroll
     for (int i = 0; i < Q; ++i) {
-        uint32_t e = 0, sg = 0;
-#pragma unroll
-        for (int t = 0; t < kMaxTerms; ++t) {
-            if (t < a.terms) {
-                const size_t at = t * term_stride + (size_t)i * a.N * NG + off;
-                e |= (uint32_t)reinterpret_cast<const uint8_t*>(a.exps)[at] << (8 * t);
-                sg |= (uint32_t)reinterpret_cast<const uint8_t*>(a.term_signs)[at] << (8 * t);
-            }
-        }
-        j.et[i] = e;
-        j.st[i] = sg;
+        j.et[i] = load_terms(a.exps + i * plane + off, a.terms);
+        j.st[i] = load_terms(a.term_signs + i * plane + off, a.terms);
     }
 }
 
@@ -368,6 +368,11 @@ template <int Q>
 __device__ inline void pin_plane(JobRegs<Q>& j, int i) {
     asm volatile("" : "+v"(j.w[i].x), "+v"(j.w[i].y), "+v"(j.w[i].z), "+v"(j.w[i].w),
                  "+v"(j.e[i]));
+}
+
+template <int Q>
+__device__ inline void pin_terms(JobRegs<Q>& j, int i) {
+    asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
 }
 
 // Queries and adds of one job: sum over planes of ldexp(block sum, exponent).
@@ -421,6 +426,7 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
         if constexpr (BLK) {
             tot += acc;
         } else if (terms > 0) {
+            pin_terms<Q>(j, i);
 #pragma unroll
             for (int t = 0; t < kMaxTerms; ++t) {
                 const int sg = (int)(int8_t)(j.st[i] >> (8 * t));
@@ -1315,6 +1321,10 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
     if (st != SA_OK) return st;
     if (group % 128) return SA_ERR_GROUP;
     if (terms < 1 || terms > SA_MAX_TERMS) return SA_ERR_SHAPE;
+    // the T bytes of a group are loaded at once: 2- and 4-byte loads need that alignment
+    const uintptr_t al = terms == 2 ? 1u : (terms == 4 ? 3u : 0u);
+    if ((reinterpret_cast<uintptr_t>(exps) & al) || (reinterpret_cast<uintptr_t>(term_signs) & al))
+        return SA_ERR_ALIGN;
     sa_plan plan;
     make_plan(q, N, K, group, 1, &plan);  // the row kernel's geometry
     RowsArgs a{};

@@ -278,12 +278,12 @@ def quantize_bcq(w: torch.Tensor, q: int, group: int, cycles: int, stream=None):
 
 def quantize_bcq_terms(w: torch.Tensor, q: int, group: int, cycles: int, terms: int,
                        stream=None):
-    """``(signs [q][N][K], exps [terms][q][N][K/group], term_signs [terms][q][N][K/group])``
+    """``(signs [q][N][K], exps [q][N][K/group][terms], term_signs [q][N][K/group][terms])``
     (int8, new device tensors) with additive PoT scales."""
     N, K = w.shape
     signs = torch.empty((q, N, K), dtype=torch.int8, device=w.device)
-    exps = torch.empty((terms, q, N, K // group), dtype=torch.int8, device=w.device)
-    tsg = torch.empty((terms, q, N, K // group), dtype=torch.int8, device=w.device)
+    exps = torch.empty((q, N, K // group, terms), dtype=torch.int8, device=w.device)
+    tsg = torch.empty((q, N, K // group, terms), dtype=torch.int8, device=w.device)
     sa_quantize_bcq_terms(w, N, K, q, group, cycles, terms, signs, exps, tsg, stream)
     return signs, exps, tsg
 

@@ -288,7 +288,7 @@ def test_quantize_terms_one_term_is_quantize():
     w = workloads.fp_weights(16, 512, seed=5)
     s1, e1 = bcq.quantize(w, 3, 128, 2)
     s, e, t = bcq.quantize_terms(w, 3, 128, 2, 1)
-    assert np.array_equal(s, s1) and np.array_equal(e[0], e1)
+    assert np.array_equal(s, s1) and np.array_equal(e[..., 0], e1)
     assert set(np.unique(t)) <= {0, 1}
 
 
@@ -297,7 +297,7 @@ def test_quantize_terms_format_and_error():
     errs = []
     for T in (1, 2, 3):
         s, e, t = bcq.quantize_terms(w, 3, 128, 2, T)
-        assert (t[0] >= 0).all() and set(np.unique(t)) <= {-1, 0, 1}
+        assert (t[..., 0] >= 0).all() and set(np.unique(t)) <= {-1, 0, 1}
         B, pa = bcq.quantize_segments(bcq.segments(w, 128), 3, 2, terms=T)
         direct = np.einsum("si,sig->sg", pa, B).reshape(w.shape)
         assert np.array_equal(bcq.reconstruct_terms(s, e, t, 128), direct)

@@ -77,8 +77,8 @@ def test_one_term_matches_row_wise_kernel():
     c = workloads.terms_case(q, N, K, G, B, 1, seed=11)
     y = run(c)
     yr = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
-    sa.sa_shiftadd_gemm(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"][0]), q, N,
-                        K, G, B, yr)
+    sa.sa_shiftadd_gemm(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"][..., 0]), q,
+                        N, K, G, B, yr)
     torch.cuda.synchronize()
     assert np.array_equal(y, yr.cpu().numpy().astype(np.float64))  # same arithmetic
 

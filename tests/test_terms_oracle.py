@@ -18,7 +18,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "terms_hand.json")
 
 
 def dense(signs, exps, term_signs, G):
-    f = (term_signs.astype(np.float64) * np.ldexp(1.0, exps.astype(np.int64))).sum(0)  # [q][N][NG]
+    f = (term_signs.astype(np.float64) * np.ldexp(1.0, exps.astype(np.int64))).sum(-1)  # [q][N][NG]
     return (signs.astype(np.float64) * np.repeat(f, G, axis=2)).sum(0)
 
 
@@ -34,25 +34,26 @@ def test_hand_example():
 def test_one_term_is_the_row_wise_layer(q, N, K, G, B):
     c = workloads.terms_case(q, N, K, G, B, 1, seed=2)
     y, a = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G)
-    y_row, a_row = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"][0], G)
+    y_row, a_row = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"][..., 0], G)
     assert np.array_equal(y, y_row) and np.array_equal(a, a_row)
 
 
 def test_sign_zero_term_is_no_term():
     c = workloads.terms_case(3, 40, 256, 128, 2, 3, seed=3)
     ts = c["term_signs"].copy()
-    ts[2] = 0
+    ts[..., 2] = 0
     y, a = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], ts, 128)
-    y2, a2 = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"][:2], ts[:2], 128)
+    y2, a2 = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"][..., :2].copy(),
+                                        ts[..., :2].copy(), 128)
     assert np.array_equal(y, y2) and np.array_equal(a, a2)
 
 
 def test_two_equal_terms_are_one_doubled_term():
     c = workloads.terms_case(2, 40, 256, 128, 2, 1, seed=4)
-    e2 = np.concatenate([c["exps"], c["exps"]])
+    e2 = np.concatenate([c["exps"], c["exps"]], axis=-1)
     s2 = np.ones_like(e2)
     y, a = oracle.shiftadd_gemm_terms(c["x"], c["signs"], e2, s2, 128)
-    y1, a1 = oracle.shiftadd_gemm(c["x"], c["signs"], (c["exps"][0] + 1).astype(np.int8), 128)
+    y1, a1 = oracle.shiftadd_gemm(c["x"], c["signs"], (c["exps"][..., 0] + 1).astype(np.int8), 128)
     assert np.abs(y - y1).max() <= 1e-12 * a.max() and np.abs(a - a1).max() <= 1e-12 * a.max()
 
 
@@ -72,8 +73,8 @@ def test_exact_rational_brute_force():
             exact = Fraction(0)
             for i in range(2):
                 for k in range(32):
-                    f = sum(Fraction(int(c["term_signs"][t, i, n, k // 8]))
-                            * Fraction(2) ** int(c["exps"][t, i, n, k // 8]) for t in range(3))
+                    f = sum(Fraction(int(c["term_signs"][i, n, k // 8, t]))
+                            * Fraction(2) ** int(c["exps"][i, n, k // 8, t]) for t in range(3))
                     exact += Fraction(int(c["signs"][i, n, k])) * Fraction(float(c["x"][b, k])) * f
             assert abs(Fraction(y[b, n]) - exact) <= Fraction(2) ** -50 * (abs(exact) + 1)
 
@@ -86,8 +87,8 @@ def test_planted_mistakes_fail_the_dense_pin(mistake):
     if mistake == "signs_ignored":
         ts = np.abs(ts)
     elif mistake == "first_term_only":
-        ts[1:] = 0
+        ts[..., 1:] = 0
     else:
-        e[1] = e[1][::-1]
+        e[..., 1] = e[::-1, ..., 1]
     bad = c["x"].astype(np.float64) @ dense(c["signs"], e, ts, 128).T
     assert np.abs(y - bad).max() > 1e-3 * a.max()

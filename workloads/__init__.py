@@ -287,9 +287,9 @@ def terms_case(q: int, N: int, K: int, G: int, B: int, T: int, seed: int = 0,
                exp_range: Tuple[int, int] = (-10, -3), outlier_fraction: float = 0.01,
                outlier_scale: float = 20.0, copy: int = 0) -> dict:
     """A seeded layer with additive power-of-two factors (Eq. 2, T terms):
-    signs [q][N][K]; exps int8 [T][q][N][K/G] where term t is drawn below the
+    signs [q][N][K]; exps int8 [q][N][K/G][T] where term t is drawn below the
     previous one (term 0 uniform over the range, term t = term t-1 minus 1..3,
-    as a greedy residual expansion would give); term signs int8 [T][q][N][K/G]:
+    as a greedy residual expansion would give); term signs int8 [q][N][K/G][T]:
     term 0 is +1 (its sign is folded into the plane), later terms are +-1 or, one
     time in eight, 0 (no term).  Draw order: signs, exps, term signs, x,
     outlier channels."""
@@ -308,6 +308,8 @@ def terms_case(q: int, N: int, K: int, G: int, B: int, T: int, seed: int = 0,
         exps[t] = e0
     tsg = rng.choice(np.array([-1, 1, 1, 1, -1, 1, -1, 0], dtype=np.int8), size=(T, q, N, NG))
     tsg[0] = 1
+    exps = np.ascontiguousarray(exps.transpose(1, 2, 3, 0))   # term index last
+    tsg = np.ascontiguousarray(tsg.transpose(1, 2, 3, 0))
     x16, idx = _draw_x(rng, K, B, outlier_fraction, outlier_scale)
     return dict(signs=signs, exps=exps, term_signs=tsg, x=x16, outlier_channels=idx, q=q, N=N,
                 K=K, G=G, B=B, T=T, name=f"terms(q={q},N={N},K={K},G={G},B={B},T={T})",
