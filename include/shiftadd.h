@@ -255,6 +255,64 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t *x, const uint8_t *packed_bits,
 /* Launch geometry of sa_shiftadd_gemm_blockwise (host-only). */
 SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch, sa_plan *plan);
 
+/* ---- Automated mixed-bit allocation (Sec. 4.3, Eq. 3 and Eq. 4) ----
+ *
+ * The criterion of a layer, C = ||IS||_F STD(IS)^2 with IS = W /
+ * diag(cholesky(H^-1)) and H = X X^T + damp * mean(diag(X X^T)) I (X the
+ * calibration activations, one column per token), is computed in three calls:
+ * sa_gram_f16 (X X^T), sa_inverse_cholesky_diag (the diagonal of the Cholesky
+ * factor of H^-1), sa_importance_criterion (C).  The caller owns every buffer,
+ * workspaces included; nothing is allocated. */
+
+/* H = X X^T (Eq. 3) on the matrix cores, fp32 accumulation of fp16 products.
+ *   x  (device) fp16 bits [K][T] row-major (one row per input channel), 16-byte
+ *      aligned; K % 64 == 0, T % 32 == 0 (pad with zero tokens; they add nothing).
+ *   H  (device) fp32 [K][K], fully overwritten (symmetric).
+ * Asynchronous on `stream`. */
+SA_API int sa_gram_f16(const uint16_t *x, int K, int T, float *H, void *stream);
+
+/* d[k] = diag(cholesky((H + damp * mean(diag H) I)^-1))[k] in fp64 (Eq. 3).
+ * Computed without forming the inverse: the Cholesky factor of H^-1 has, in
+ * reverse order, the reciprocals of the diagonal of the Cholesky factor of the
+ * matrix with rows and columns reversed, which is factored here (blocked, 64
+ * columns per panel).  A matrix that is not positive definite after damping
+ * yields NaN entries.
+ *   H  (device) fp32 [K][K] symmetric (only its lower triangle is read).
+ *   damp >= 0.  d (device) fp64 [K], 8-byte aligned.
+ *   workspace (device) >= sa_inverse_cholesky_workspace(K) bytes, 256-byte
+ *      aligned, owned by the caller (its contents are overwritten).
+ * Asynchronous on `stream`. */
+SA_API size_t sa_inverse_cholesky_workspace(int K);
+SA_API int sa_inverse_cholesky_diag(const float *H, int K, double damp, double *d,
+                                    void *workspace, size_t workspace_bytes, void *stream);
+
+/* out[0] = C = ||IS||_F * STD(IS)^2, out[1] = ||IS||_F, out[2] = STD(IS)
+ * (population standard deviation over all N*K entries), IS[n][k] = w[n][k] /
+ * d[k], fp64 sums in a fixed order (Eq. 3).
+ *   w (device) fp32 [N][K]; d (device) fp64 [K]; out (device) fp64 [3].
+ *   workspace (device) >= sa_importance_workspace() bytes, 8-byte aligned. */
+SA_API size_t sa_importance_workspace(void);
+SA_API int sa_importance_criterion(const float *w, int N, int K, const double *d, double *out,
+                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/* Host only.  Per-bit estimates C_{i,b}: for each bit width (column b of
+ * errors [L][nb], the measured reparameterization errors of L calibration
+ * layers) the least-squares polynomial of the given degree in the criterion
+ * c[L] is fitted, and out[i][b] = p_b(c[i]) (Sec. 4.3).  Needs L > degree and
+ * degree + 1 distinct criteria (else SA_ERR_SHAPE). */
+SA_API int sa_fit_per_bit(const double *c, const double *errors, int L, int nb, int degree,
+                          double *out);
+
+/* Host only.  Eq. 4: one bit width per layer, out[i] in bits[], minimising
+ * sum_i cost[i][b_i] (summed from layer 0) subject to sum_i b_i <= budget * L,
+ * exactly (a multiple-choice knapsack over integer bit totals by dynamic
+ * programming).  Ties: fewer total bits, then the lexicographically smallest
+ * widths (layer 0 first).  cost [L][nb], bits [nb] in [1, 64], nb <= 16.
+ * *objective (may be NULL) receives the minimum.  SA_ERR_SHAPE when nothing
+ * fits the budget. */
+SA_API int sa_allocate_bits(const double *cost, const int *bits, int L, int nb, double budget,
+                            int *out, double *objective);
+
 /* Measurement aid, not part of the layer (no operation of the paper): reads
  * every byte of `buf` once -- each thread three 16-byte words, grid-strided, so
  * every wave request is 1 KiB of contiguous memory -- and writes at most one

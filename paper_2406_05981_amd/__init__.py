@@ -11,7 +11,8 @@ __all__ = [
     "sa_plan_gemm_colwise", "sa_quantize_bcq", "sa_read_probe", "sa_status_string",
     "sa_version", "quantize_bcq", "shiftadd_gemm_colwise", "sa_shiftadd_gemm_blockwise",
     "sa_plan_gemm_blockwise", "shiftadd_gemm_blockwise", "sa_shiftadd_gemm_terms",
-    "sa_quantize_bcq_terms", "quantize_bcq_terms",
+    "sa_quantize_bcq_terms", "quantize_bcq_terms", "sa_gram_f16", "sa_inverse_cholesky_diag",
+    "sa_importance_criterion", "sa_fit_per_bit", "sa_allocate_bits", "bit_criterion",
     "pack_weights", "shiftadd_gemm", "SaError",
 ]
 

@@ -11,7 +11,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "shiftadd.hip"), os.path.join(HERE, "csrc", "bcq.hip")]
+SOURCES = [os.path.join(HERE, "csrc", "shiftadd.hip"), os.path.join(HERE, "csrc", "bcq.hip"),
+           os.path.join(HERE, "csrc", "alloc.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libshiftadd.so")
 ARCH = "gfx950"

@@ -1,0 +1,511 @@
+// gfx950 kernels and C ABI of the automated mixed-bit allocation of ShiftAddLLM
+// (Sec. 4.3): the criterion of Eq. 3 for one layer, the per-bit least-squares
+// fits, and the integer program of Eq. 4.
+//
+//   IS = W / diag(cholesky(H^-1)),  H = X X^T + damp * mean(diag(X X^T)) I,
+//   C  = ||IS||_F * STD(IS)^2
+//
+// computed as: the Gram matrix X X^T of fp16 calibration activations on the
+// matrix cores (v_mfma_f32_16x16x16_f16, fp32 accumulation; only the lower
+// triangle of tiles); the damped matrix in fp64 with rows and columns in reverse
+// order; a blocked fp64 Cholesky of it, because the diagonal of the Cholesky
+// factor of H^-1 is, in reverse order, the reciprocal of the diagonal of the
+// Cholesky factor of the reversed H (no inverse is formed); and fp64 sums of IS
+// and IS^2 in a fixed order.  Eq. 4 is a multiple-choice knapsack over integer
+// bit totals, solved exactly on the host.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "shiftadd.h"
+
+namespace {
+
+// ---------------------------------------------------------------- Gram matrix
+
+constexpr int kGT = 64;        // output tile: 64 x 64
+constexpr int kGK = 32;        // calibration columns per step
+constexpr int kGPad = kGK + 4; // LDS row stride in halves (72 bytes): spreads rows over banks
+
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+// Tile (ti, tj), ti >= tj, of H = X X^T for X fp16 [K][T] row-major.  Four
+// waves, each a 32 x 32 quarter (2 x 2 blocks of 16 x 16).  Per step the two
+// 64 x 32 slices of X are staged in LDS; one MFMA consumes 16 columns.
+// Operand layout of v_mfma_f32_16x16x16_f16: lane l holds row (l mod 16) of A
+// and column (l mod 16) of B at k = 4 (l / 16) .. 4 (l / 16) + 3; the result
+// holds rows 4 (l / 16) .. + 3 of column (l mod 16).
+__global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x, int K, int T,
+                                                  float* __restrict__ H) {
+    __shared__ uint16_t sa[kGT * kGPad];
+    __shared__ uint16_t sb[kGT * kGPad];
+    // linear block index -> lower-triangular tile (ti >= tj)
+    const int b = blockIdx.x;
+    int ti = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
+    while ((ti + 1) * (ti + 2) / 2 <= b) ++ti;
+    while (ti * (ti + 1) / 2 > b) --ti;
+    const int tj = b - ti * (ti + 1) / 2;
+    const int i0 = ti * kGT, j0 = tj * kGT;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;
+    // staging: thread -> (row, 8 halves)
+    const int lr = tid >> 2, lc = (tid & 3) * 8;
+    const uint16_t* pa = x + (int64_t)(i0 + lr) * T + lc;
+    const uint16_t* pb = x + (int64_t)(j0 + lr) * T + lc;
+    float4v acc[2][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int v = 0; v < 2; ++v) acc[u][v] = float4v{0.f, 0.f, 0.f, 0.f};
+    const int r16 = lane & 15, kq = (lane >> 4) * 4;
+    for (int t0 = 0; t0 < T; t0 += kGK) {
+        const uint4 va = *reinterpret_cast<const uint4*>(pa + t0);
+        const uint4 vb = *reinterpret_cast<const uint4*>(pb + t0);
+        __syncthreads();  // the previous step's reads are done
+        *reinterpret_cast<uint2*>(sa + lr * kGPad + lc) = make_uint2(va.x, va.y);
+        *reinterpret_cast<uint2*>(sa + lr * kGPad + lc + 4) = make_uint2(va.z, va.w);
+        *reinterpret_cast<uint2*>(sb + lr * kGPad + lc) = make_uint2(vb.x, vb.y);
+        *reinterpret_cast<uint2*>(sb + lr * kGPad + lc + 4) = make_uint2(vb.z, vb.w);
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < kGK; ks += 16) {
+            half4 av[2], bv[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const uint2 ra = *reinterpret_cast<const uint2*>(sa + (wi + 16 * u + r16) * kGPad + ks + kq);
+                const uint2 rb = *reinterpret_cast<const uint2*>(sb + (wj + 16 * u + r16) * kGPad + ks + kq);
+                av[u] = __builtin_bit_cast(half4, ra);
+                bv[u] = __builtin_bit_cast(half4, rb);
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int v = 0; v < 2; ++v)
+                    acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x16f16(av[u], bv[v], acc[u][v], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int v = 0; v < 2; ++v)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int i = i0 + wi + 16 * u + (lane >> 4) * 4 + e;
+                const int j = j0 + wj + 16 * v + r16;
+                H[(int64_t)i * K + j] = acc[u][v][e];
+                if (ti != tj) H[(int64_t)j * K + i] = acc[u][v][e];
+            }
+}
+
+// ---------------------------------------------------------------- damping, reversal
+
+// lambda = damp * mean(diag(H)) (fp64, one workgroup, fixed order).
+__global__ __launch_bounds__(256) void k_damping(const float* __restrict__ H, int K, double damp,
+                                                 double* __restrict__ lambda) {
+    __shared__ double part[256];
+    double s = 0.0;
+    for (int k = threadIdx.x; k < K; k += 256) s += (double)H[(int64_t)k * K + k];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *lambda = damp * (part[0] / K);
+}
+
+// A = J H J + lambda I in fp64 (lower triangle and diagonal), J the reversal.
+__global__ __launch_bounds__(256) void k_reverse(const float* __restrict__ H, int K,
+                                                 const double* __restrict__ lambda,
+                                                 double* __restrict__ A) {
+    const int64_t n = (int64_t)K * K;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
+        const int i = (int)(e / K), j = (int)(e % K);
+        if (j > i) continue;
+        double v = (double)H[(int64_t)(K - 1 - j) * K + (K - 1 - i)];
+        if (i == j) v += *lambda;
+        A[e] = v;
+    }
+}
+
+// ---------------------------------------------------------------- blocked Cholesky (fp64, lower)
+
+constexpr int kNB = 64;             // panel width
+constexpr int kNBP = kNB + 1;       // LDS row stride (doubles)
+
+// Diagonal block [j, j + 64) factored in place (unblocked, right-looking).  A
+// non-positive pivot gives NaN, which then runs through every later value.
+__global__ __launch_bounds__(256) void k_chol_diag(double* __restrict__ A, int K, int j) {
+    __shared__ double a[kNB * kNBP];
+    const int nb = min(kNB, K - j);
+    for (int e = threadIdx.x; e < nb * nb; e += 256) {
+        const int r = e / nb, c = e % nb;
+        a[r * kNBP + c] = c <= r ? A[(int64_t)(j + r) * K + j + c] : 0.0;
+    }
+    __syncthreads();
+    for (int c = 0; c < nb; ++c) {
+        if (threadIdx.x == 0) a[c * kNBP + c] = sqrt(a[c * kNBP + c]);
+        __syncthreads();
+        const double p = a[c * kNBP + c];
+        for (int r = c + 1 + threadIdx.x; r < nb; r += 256) a[r * kNBP + c] /= p;
+        __syncthreads();
+        const int m = nb - c - 1;  // trailing lower triangle, m (m + 1) / 2 entries
+        for (int e = threadIdx.x; e < m * m; e += 256) {
+            const int r = c + 1 + e / m, s = c + 1 + e % m;
+            if (s <= r) a[r * kNBP + s] -= a[r * kNBP + c] * a[s * kNBP + c];
+        }
+        __syncthreads();
+    }
+    for (int e = threadIdx.x; e < nb * nb; e += 256) {
+        const int r = e / nb, c = e % nb;
+        if (c <= r) A[(int64_t)(j + r) * K + j + c] = a[r * kNBP + c];
+    }
+}
+
+// Panel below the diagonal block: row r (r >= j + 64) solves x L11^T = a.  One
+// thread per row; L11 and the 64 rows of the workgroup staged in LDS.
+__global__ __launch_bounds__(64) void k_chol_trsm(double* __restrict__ A, int K, int j) {
+    __shared__ double l11[kNB * kNBP];
+    __shared__ double rows[kNB * kNBP];
+    const int r0 = j + kNB + blockIdx.x * kNB;
+    for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
+        const int r = e / kNB, c = e % kNB;
+        l11[r * kNBP + c] = c <= r ? A[(int64_t)(j + r) * K + j + c] : 0.0;
+        rows[r * kNBP + c] = r0 + r < K ? A[(int64_t)(r0 + r) * K + j + c] : 0.0;
+    }
+    __syncthreads();
+    double* xr = rows + threadIdx.x * kNBP;
+    for (int c = 0; c < kNB; ++c) {
+        double v = xr[c];
+        for (int k = 0; k < c; ++k) v -= xr[k] * l11[c * kNBP + k];
+        xr[c] = v / l11[c * kNBP + c];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
+        const int r = e / kNB, c = e % kNB;
+        if (r0 + r < K) A[(int64_t)(r0 + r) * K + j + c] = rows[r * kNBP + c];
+    }
+}
+
+// Trailing update of the lower triangle: A[r][s] -= sum_c L[r][c] L[s][c] over
+// the panel's 64 columns, for 64 x 64 tiles (tr >= ts) below the panel.  Each
+// thread owns a 4 x 4 block of the tile.
+__global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K, int j) {
+    __shared__ double lr_[kNB * kNBP];
+    __shared__ double ls_[kNB * kNBP];
+    const int b = blockIdx.x;
+    int tr = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
+    while ((tr + 1) * (tr + 2) / 2 <= b) ++tr;
+    while (tr * (tr + 1) / 2 > b) --tr;
+    const int ts = b - tr * (tr + 1) / 2;
+    const int base = j + kNB;
+    const int r0 = base + tr * kNB, s0 = base + ts * kNB;
+    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+        const int r = e / kNB, c = e % kNB;
+        lr_[r * kNBP + c] = r0 + r < K ? A[(int64_t)(r0 + r) * K + j + c] : 0.0;
+        ls_[r * kNBP + c] = s0 + r < K ? A[(int64_t)(s0 + r) * K + j + c] : 0.0;
+    }
+    __syncthreads();
+    const int rr = (threadIdx.x >> 4) * 4, ss = (threadIdx.x & 15) * 4;
+    double acc[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
+    for (int c = 0; c < kNB; ++c) {
+        double a4[4], b4[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a4[u] = lr_[(rr + u) * kNBP + c];
+            b4[u] = ls_[(ss + u) * kNBP + c];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[u][v] = fma(a4[u], b4[v], acc[u][v]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int r = r0 + rr + u, s = s0 + ss + v;
+            if (r < K && s < K && s <= r) A[(int64_t)r * K + s] -= acc[u][v];
+        }
+}
+
+// d[k] = 1 / L[K-1-k][K-1-k]: the diagonal of the Cholesky factor of H^-1.
+__global__ __launch_bounds__(256) void k_inverse_diag(const double* __restrict__ A, int K,
+                                                      double* __restrict__ d) {
+    const int k = blockIdx.x * 256 + threadIdx.x;
+    if (k < K) d[k] = 1.0 / A[(int64_t)(K - 1 - k) * K + (K - 1 - k)];
+}
+
+// ---------------------------------------------------------------- criterion
+
+constexpr int kStatBlocks = 1024;
+
+// Per-block fp64 sums of IS and IS^2 (grid-strided, fixed order per block).
+__global__ __launch_bounds__(256) void k_is_partials(const float* __restrict__ w, int N, int K,
+                                                     const double* __restrict__ d,
+                                                     double* __restrict__ part) {
+    __shared__ double s1[256], s2[256];
+    const int64_t n = (int64_t)N * K;
+    double a = 0.0, b = 0.0;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
+        const double v = (double)w[e] / d[e % K];
+        a += v;
+        b += v * v;
+    }
+    s1[threadIdx.x] = a;
+    s2[threadIdx.x] = b;
+    __syncthreads();
+    for (int m = 128; m >= 1; m >>= 1) {
+        if ((int)threadIdx.x < m) {
+            s1[threadIdx.x] += s1[threadIdx.x + m];
+            s2[threadIdx.x] += s2[threadIdx.x + m];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        part[2 * blockIdx.x] = s1[0];
+        part[2 * blockIdx.x + 1] = s2[0];
+    }
+}
+
+// out[0] = C = ||IS||_F STD(IS)^2, out[1] = ||IS||_F, out[2] = STD(IS).
+__global__ __launch_bounds__(256) void k_is_final(const double* __restrict__ part, int nparts,
+                                                  int64_t n, double* __restrict__ out) {
+    __shared__ double s1[256], s2[256];
+    double a = 0.0, b = 0.0;
+    for (int p = threadIdx.x; p < nparts; p += 256) {
+        a += part[2 * p];
+        b += part[2 * p + 1];
+    }
+    s1[threadIdx.x] = a;
+    s2[threadIdx.x] = b;
+    __syncthreads();
+    for (int m = 128; m >= 1; m >>= 1) {
+        if ((int)threadIdx.x < m) {
+            s1[threadIdx.x] += s1[threadIdx.x + m];
+            s2[threadIdx.x] += s2[threadIdx.x + m];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double mean = s1[0] / (double)n;
+        const double var = fmax(s2[0] / (double)n - mean * mean, 0.0);
+        const double fro = sqrt(s2[0]);
+        out[0] = fro * var;
+        out[1] = fro;
+        out[2] = sqrt(var);
+    }
+}
+
+int status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+}  // namespace
+
+// ---------------------------------------------------------------- C ABI
+
+SA_API int sa_gram_f16(const uint16_t* x, int K, int T, float* H, void* stream) {
+    if (!x || !H) return SA_ERR_NULL;
+    if (K < kGT || (K % kGT) || T < kGK || (T % kGK) || (int64_t)K * T > ((int64_t)1 << 40))
+        return SA_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(x) & 15u) || (reinterpret_cast<uintptr_t>(H) & 3u))
+        return SA_ERR_ALIGN;
+    const int tiles = K / kGT;
+    hipLaunchKernelGGL(k_gram_f16, dim3(tiles * (tiles + 1) / 2), dim3(256), 0,
+                       reinterpret_cast<hipStream_t>(stream), x, K, T, H);
+    return status();
+}
+
+SA_API size_t sa_inverse_cholesky_workspace(int K) {
+    if (K < 1) return 0;
+    return align256((size_t)K * K * sizeof(double)) + 256;
+}
+
+SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* d,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+    if (!H || !d || !workspace) return SA_ERR_NULL;
+    if (K < 1 || K > 65536 || !(damp >= 0.0)) return SA_ERR_SHAPE;
+    if (workspace_bytes < sa_inverse_cholesky_workspace(K)) return SA_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) || (reinterpret_cast<uintptr_t>(d) & 7u))
+        return SA_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    double* A = static_cast<double*>(workspace);
+    double* lambda = reinterpret_cast<double*>(static_cast<char*>(workspace) +
+                                               align256((size_t)K * K * sizeof(double)));
+    hipLaunchKernelGGL(k_damping, dim3(1), dim3(256), 0, s, H, K, damp, lambda);
+    const int64_t n = (int64_t)K * K;
+    const int grid = (int)(((n + 255) / 256) < 8192 ? (n + 255) / 256 : 8192);
+    hipLaunchKernelGGL(k_reverse, dim3(grid), dim3(256), 0, s, H, K, lambda, A);
+    for (int j = 0; j < K; j += kNB) {
+        hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(256), 0, s, A, K, j);
+        const int below = K - j - kNB;
+        if (below > 0) {
+            const int rb = (below + kNB - 1) / kNB;
+            hipLaunchKernelGGL(k_chol_trsm, dim3(rb), dim3(64), 0, s, A, K, j);
+            hipLaunchKernelGGL(k_chol_syrk, dim3(rb * (rb + 1) / 2), dim3(256), 0, s, A, K, j);
+        }
+    }
+    hipLaunchKernelGGL(k_inverse_diag, dim3((K + 255) / 256), dim3(256), 0, s, A, K, d);
+    return status();
+}
+
+SA_API size_t sa_importance_workspace(void) { return (size_t)2 * kStatBlocks * sizeof(double); }
+
+SA_API int sa_importance_criterion(const float* w, int N, int K, const double* d, double* out,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+    if (!w || !d || !out || !workspace) return SA_ERR_NULL;
+    if (N < 1 || K < 1 || (int64_t)N * K > ((int64_t)1 << 40)) return SA_ERR_SHAPE;
+    if (workspace_bytes < sa_importance_workspace()) return SA_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 7u) || (reinterpret_cast<uintptr_t>(out) & 7u))
+        return SA_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    double* part = static_cast<double*>(workspace);
+    hipLaunchKernelGGL(k_is_partials, dim3(kStatBlocks), dim3(256), 0, s, w, N, K, d, part);
+    hipLaunchKernelGGL(k_is_final, dim3(1), dim3(256), 0, s, part, kStatBlocks, (int64_t)N * K,
+                       out);
+    return status();
+}
+
+// ---------------------------------------------------------------- host: fits and Eq. 4
+
+SA_API int sa_fit_per_bit(const double* c, const double* errors, int L, int nb, int degree,
+                          double* out) {
+    if (!c || !errors || !out) return SA_ERR_NULL;
+    if (L < 1 || nb < 1 || degree < 0 || degree > 8 || L < degree + 1) return SA_ERR_SHAPE;
+    const int m = degree + 1;
+    // least squares by the normal equations of the scaled Vandermonde system
+    // (columns c^p / s^p, s = max |c|), solved by Gaussian elimination with
+    // partial pivoting in fp64
+    double sc = 0.0;
+    for (int i = 0; i < L; ++i) sc = fmax(sc, fabs(c[i]));
+    if (sc == 0.0) sc = 1.0;
+    std::vector<double> M(m * m), v(m), coef(m);
+    for (int b = 0; b < nb; ++b) {
+        std::fill(M.begin(), M.end(), 0.0);
+        std::fill(v.begin(), v.end(), 0.0);
+        for (int i = 0; i < L; ++i) {
+            const double t = c[i] / sc;
+            double pp[9];
+            pp[0] = 1.0;
+            for (int p = 1; p < m; ++p) pp[p] = pp[p - 1] * t;
+            for (int p = 0; p < m; ++p) {
+                v[p] += pp[p] * errors[i * nb + b];
+                for (int q = 0; q < m; ++q) M[p * m + q] += pp[p] * pp[q];
+            }
+        }
+        for (int col = 0; col < m; ++col) {
+            int piv = col;
+            for (int r = col + 1; r < m; ++r)
+                if (fabs(M[r * m + col]) > fabs(M[piv * m + col])) piv = r;
+            if (M[piv * m + col] == 0.0) return SA_ERR_SHAPE;  // too few distinct criteria
+            if (piv != col) {
+                for (int q = 0; q < m; ++q) std::swap(M[piv * m + q], M[col * m + q]);
+                std::swap(v[piv], v[col]);
+            }
+            for (int r = col + 1; r < m; ++r) {
+                const double f = M[r * m + col] / M[col * m + col];
+                for (int q = col; q < m; ++q) M[r * m + q] -= f * M[col * m + q];
+                v[r] -= f * v[col];
+            }
+        }
+        for (int col = m - 1; col >= 0; --col) {
+            double acc = v[col];
+            for (int q = col + 1; q < m; ++q) acc -= M[col * m + q] * coef[q];
+            coef[col] = acc / M[col * m + col];
+        }
+        for (int i = 0; i < L; ++i) {
+            const double t = c[i] / sc;
+            double y = 0.0;
+            for (int p = m - 1; p >= 0; --p) y = y * t + coef[p];
+            out[i * nb + b] = y;
+        }
+    }
+    return SA_OK;
+}
+
+SA_API int sa_allocate_bits(const double* cost, const int* bits, int L, int nb, double budget,
+                            int* out, double* objective) {
+    if (!cost || !bits || !out) return SA_ERR_NULL;
+    if (L < 1 || nb < 1 || nb > 16 || L > 100000) return SA_ERR_SHAPE;
+    int bmax = 0;
+    for (int k = 0; k < nb; ++k) {
+        if (bits[k] < 1 || bits[k] > 64) return SA_ERR_SHAPE;
+        bmax = bits[k] > bmax ? bits[k] : bmax;
+    }
+    // a total t is allowed when t <= budget * L in fp64, i.e. t <= floor(budget * L)
+    const double capd = floor(budget * (double)L);
+    if (!(capd >= 0.0)) return SA_ERR_SHAPE;
+    const int64_t cap = (int64_t)fmin(capd, (double)bmax * L);
+    const int64_t W = cap + 1;
+    // f[l][t]: the best prefix over layers 0..l-1 using exactly t bits -- the
+    // smallest objective (summed from layer 0), then the lexicographically
+    // smallest widths; choice[l][t] is the last layer's option of that prefix.
+    const double INF = INFINITY;
+    std::vector<double> f((size_t)(L + 1) * W, INF);
+    std::vector<int8_t> choice((size_t)(L + 1) * W, -1);
+    f[0] = 0.0;
+    auto lex_less = [&](int l, int64_t t1, int k1, int64_t t2, int k2) {
+        // compare the widths of prefix (l, t1 via k1) with (l, t2 via k2), both of l + 1 layers
+        std::vector<int> a(l + 1), b(l + 1);
+        int64_t u = t1;
+        a[l] = bits[k1];
+        u -= bits[k1];
+        for (int m = l - 1; m >= 0; --m) {
+            const int k = choice[(size_t)(m + 1) * W + u];
+            a[m] = bits[k];
+            u -= bits[k];
+        }
+        u = t2;
+        b[l] = bits[k2];
+        u -= bits[k2];
+        for (int m = l - 1; m >= 0; --m) {
+            const int k = choice[(size_t)(m + 1) * W + u];
+            b[m] = bits[k];
+            u -= bits[k];
+        }
+        return a < b;
+    };
+    for (int l = 0; l < L; ++l) {
+        for (int64_t t = 0; t < W; ++t) {
+            const double base = f[(size_t)l * W + t];
+            if (base == INF) continue;
+            for (int k = 0; k < nb; ++k) {
+                const int64_t t2 = t + bits[k];
+                if (t2 >= W) continue;
+                const double v = base + cost[(size_t)l * nb + k];
+                double& cur = f[(size_t)(l + 1) * W + t2];
+                int8_t& ch = choice[(size_t)(l + 1) * W + t2];
+                if (v < cur || (v == cur && ch >= 0 && lex_less(l, t2, k, t2, ch))) {
+                    cur = v;
+                    ch = (int8_t)k;
+                }
+            }
+        }
+    }
+    int64_t best_t = -1;
+    for (int64_t t = 0; t < W; ++t) {
+        const double v = f[(size_t)L * W + t];
+        if (v == INF) continue;
+        if (best_t < 0 || v < f[(size_t)L * W + best_t]) best_t = t;  // ties: fewer bits
+    }
+    if (best_t < 0) return SA_ERR_SHAPE;  // nothing fits the budget
+    int64_t u = best_t;
+    for (int l = L - 1; l >= 0; --l) {
+        const int k = choice[(size_t)(l + 1) * W + u];
+        out[l] = bits[k];
+        u -= bits[k];
+    }
+    if (objective) *objective = f[(size_t)L * W + best_t];
+    return SA_OK;
+}

@@ -53,6 +53,13 @@ def _bind(lib):
         "sa_read_probe": ([P, ctypes.c_size_t, P, P], I),
         "sa_quantize_bcq": ([P, I, I, I, I, I, P, P, P], I),
         "sa_quantize_bcq_terms": ([P, I, I, I, I, I, I, P, P, P, P], I),
+        "sa_gram_f16": ([P, I, I, P, P], I),
+        "sa_inverse_cholesky_workspace": ([I], ctypes.c_size_t),
+        "sa_inverse_cholesky_diag": ([P, I, ctypes.c_double, P, P, ctypes.c_size_t, P], I),
+        "sa_importance_workspace": ([], ctypes.c_size_t),
+        "sa_importance_criterion": ([P, I, I, P, P, P, ctypes.c_size_t, P], I),
+        "sa_fit_per_bit": ([P, P, I, I, I, P], I),
+        "sa_allocate_bits": ([P, P, I, I, ctypes.c_double, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
         "sa_version": ([], ctypes.c_char_p),
     }
@@ -253,6 +260,57 @@ def sa_quantize_bcq_terms(w: torch.Tensor, N: int, K: int, q: int, group: int, c
         _stream(stream)), "sa_quantize_bcq_terms")
 
 
+def sa_gram_f16(x: torch.Tensor, K: int, T: int, H: torch.Tensor, stream=None) -> None:
+    _check(lib.sa_gram_f16(_dev(x, "x", torch.float16, K * T), K, T,
+                           _dev(H, "H", torch.float32, K * K), _stream(stream)), "sa_gram_f16")
+
+
+def sa_inverse_cholesky_diag(H: torch.Tensor, K: int, damp: float, d: torch.Tensor,
+                             workspace: torch.Tensor, stream=None) -> None:
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib.sa_inverse_cholesky_diag(_dev(H, "H", torch.float32, K * K), K, float(damp),
+                                        _dev(d, "d", torch.float64, K),
+                                        _dev(workspace, "workspace", workspace.dtype,
+                                             workspace.numel()), nbytes, _stream(stream)),
+           "sa_inverse_cholesky_diag")
+
+
+def sa_importance_criterion(w: torch.Tensor, N: int, K: int, d: torch.Tensor, out: torch.Tensor,
+                            workspace: torch.Tensor, stream=None) -> None:
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib.sa_importance_criterion(_dev(w, "w", torch.float32, N * K), N, K,
+                                       _dev(d, "d", torch.float64, K),
+                                       _dev(out, "out", torch.float64, 3),
+                                       _dev(workspace, "workspace", workspace.dtype,
+                                            workspace.numel()), nbytes, _stream(stream)),
+           "sa_importance_criterion")
+
+
+def sa_fit_per_bit(c, errors, degree: int = 1):
+    """Host: per-bit least-squares polynomial estimates ``[L][nb]`` (numpy in and out)."""
+    import numpy as np
+    c = np.ascontiguousarray(c, dtype=np.float64)
+    errors = np.ascontiguousarray(errors, dtype=np.float64)
+    L, nb = errors.shape
+    out = np.empty((L, nb), dtype=np.float64)
+    _check(lib.sa_fit_per_bit(c.ctypes.data, errors.ctypes.data, L, nb, degree, out.ctypes.data),
+           "sa_fit_per_bit")
+    return out
+
+
+def sa_allocate_bits(cost, bits, budget: float):
+    """Host: Eq. 4 -> ``(widths [L] int, objective)`` (numpy in and out)."""
+    import numpy as np
+    cost = np.ascontiguousarray(cost, dtype=np.float64)
+    L, nb = cost.shape
+    b = np.ascontiguousarray(bits, dtype=np.int32)
+    out = np.empty(L, dtype=np.int32)
+    obj = ctypes.c_double()
+    _check(lib.sa_allocate_bits(cost.ctypes.data, b.ctypes.data, L, nb, float(budget),
+                                out.ctypes.data, ctypes.byref(obj)), "sa_allocate_bits")
+    return out, obj.value
+
+
 def sa_read_probe(buf: torch.Tensor, nbytes: int, out: torch.Tensor, stream=None) -> None:
     """Plain read of ``nbytes`` bytes of ``buf`` (a measurement aid, see the header)."""
     if not isinstance(buf, torch.Tensor) or not buf.is_cuda:
@@ -326,3 +384,21 @@ def shiftadd_gemm_blockwise(x: torch.Tensor, packed_bits: torch.Tensor, blk_exps
     y = out if out is not None else torch.empty((batch, N), dtype=torch.float32, device=x.device)
     sa_shiftadd_gemm_blockwise(x, packed_bits, blk_exps, q, N, K, row_block, batch, y, stream)
     return y
+
+
+def bit_criterion(w: torch.Tensor, x: torch.Tensor, damp: float = 0.01, stream=None):
+    """Eq. 3 for one layer: ``(C, ||IS||_F, STD(IS), d)`` from fp32 weights
+    ``[N][K]`` and fp16 calibration activations ``[K][T]`` on the device
+    (workspaces are new device tensors)."""
+    N, K = w.shape
+    T = x.shape[1]
+    H = torch.empty((K, K), dtype=torch.float32, device=w.device)
+    sa_gram_f16(x, K, T, H, stream)
+    d = torch.empty(K, dtype=torch.float64, device=w.device)
+    ws = torch.empty(lib.sa_inverse_cholesky_workspace(K), dtype=torch.uint8, device=w.device)
+    sa_inverse_cholesky_diag(H, K, damp, d, ws, stream)
+    out = torch.empty(3, dtype=torch.float64, device=w.device)
+    ws2 = torch.empty(lib.sa_importance_workspace(), dtype=torch.uint8, device=w.device)
+    sa_importance_criterion(w, N, K, d, out, ws2, stream)
+    o = out.cpu()
+    return float(o[0]), float(o[1]), float(o[2]), d

@@ -254,3 +254,20 @@ def test_quantize_terms_validation_codes():
     assert call(q=9) == sa.SA_ERR_Q
     assert call(G=96) == sa.SA_ERR_GROUP
     assert call(w=A + 8) == sa.SA_ERR_ALIGN
+
+
+def test_alloc_validation_codes():
+    L = sa.lib
+    assert L.sa_gram_f16(None, 64, 32, A, None) == sa.SA_ERR_NULL
+    assert L.sa_gram_f16(A, 100, 32, A, None) == sa.SA_ERR_SHAPE     # K % 64
+    assert L.sa_gram_f16(A, 64, 40, A, None) == sa.SA_ERR_SHAPE      # T % 32
+    assert L.sa_gram_f16(A + 8, 64, 32, A, None) == sa.SA_ERR_ALIGN
+    ws = L.sa_inverse_cholesky_workspace(64)
+    assert ws >= 64 * 64 * 8
+    assert L.sa_inverse_cholesky_diag(A, 64, 0.01, A, None, ws, None) == sa.SA_ERR_NULL
+    assert L.sa_inverse_cholesky_diag(A, 64, 0.01, A, A, ws - 1, None) == sa.SA_ERR_SHAPE
+    assert L.sa_inverse_cholesky_diag(A, 64, -1.0, A, A, ws, None) == sa.SA_ERR_SHAPE
+    assert L.sa_inverse_cholesky_diag(A, 64, 0.01, A, A + 8, ws, None) == sa.SA_ERR_ALIGN
+    w2 = L.sa_importance_workspace()
+    assert L.sa_importance_criterion(A, 4, 64, A, A, A, w2 - 8, None) == sa.SA_ERR_SHAPE
+    assert L.sa_importance_criterion(A, 0, 64, A, A, A, w2, None) == sa.SA_ERR_SHAPE
