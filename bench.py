@@ -307,6 +307,110 @@ def bench_quantize(args) -> int:
     return 0
 
 
+CRIT_METRIC = "us per layer of the mixed-bit criterion (Eq. 3: Gram, Cholesky, importance)"
+F16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
+
+
+def bench_criterion(args) -> int:
+    """Times the criterion of Eq. 3 for one layer (W [N][K] fp32, calibration
+    activations X [K][T] fp16): sa_gram_f16 alone, and the whole chain (Gram,
+    damped reversed Cholesky, importance statistics)."""
+    import numpy as np
+    import torch
+
+    import workloads
+    import paper_2406_05981_amd.shiftadd as sa
+
+    N, K = args.shape
+    T = args.tokens
+    steps = args.steps if args.steps is not None else 20
+    warmup = args.warmup if args.warmup is not None else 3
+    log(f"criterion N={N} K={K} T={T}")
+    rng = np.random.default_rng(0)
+    x_np = rng.standard_normal((K, T), dtype=np.float32)
+    x_np[rng.choice(K, max(1, K // 100), replace=False)] *= 20.0
+    x = torch.from_numpy(x_np.astype(np.float16)).cuda()
+    del x_np
+    w = torch.from_numpy(workloads.fp_weights(N, K, seed=1)).cuda()
+    H = torch.empty((K, K), dtype=torch.float32, device="cuda")
+    d = torch.empty(K, dtype=torch.float64, device="cuda")
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    ws = torch.empty(sa.lib.sa_inverse_cholesky_workspace(K), dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty(sa.lib.sa_importance_workspace(), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.Stream()
+
+    def gram():
+        sa.sa_gram_f16(x, K, T, H)
+
+    def chain():
+        gram()
+        sa.sa_inverse_cholesky_diag(H, K, 0.01, d, ws)
+        sa.sa_importance_criterion(w, N, K, d, out, ws2)
+
+    def timed(fn, n):
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            for _ in range(n):
+                fn()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    us_gram = timed(gram, steps)
+    us_all = timed(chain, steps)
+    tiles = (K // 64) * (K // 64 + 1) // 2
+    flops_alg = K * (K + 1) * T          # the unique entries of X X^T, 2 flops per product
+    tflops = flops_alg / us_gram / 1e6
+    log(f"gram {us_gram:.1f} us ({tflops:.1f} TFLOP/s), whole criterion {us_all:.1f} us; "
+        f"C = {float(out[0].cpu()):.6e}")
+    res = {
+        "metric": CRIT_METRIC,
+        "value": round(us_all, 2),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": us_all / 1e3,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 products, f32 Gram, f64 Cholesky",
+        "data": "synthetic (N(0,1) fp16 calibration activations with 1% outlier channels x20; "
+                "seeded fp32 weights)",
+        "config": {"workload": f"criterion_{N}x{K}_T{T}", "N": N, "K": K, "tokens": T,
+                   "damp": 0.01, "kernel": "k_gram_f16", "gram_tiles": tiles},
+        "gram_us": round(us_gram, 2),
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2),
+                     "peak": F16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / F16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "algorithmic_flops": flops_alg},
+    }
+    if not args.no_cpu_baseline:
+        import oracle.alloc as oalloc
+        t_s = min(T, 4096)
+        xs = x[:, :t_s].cpu().numpy().astype(np.float64)
+        ws_np = w.cpu().numpy()
+        t0 = time.perf_counter()
+        oalloc.criterion(ws_np, xs, 0.01)
+        t_one = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oalloc.gram(xs)
+        t_gram = time.perf_counter() - t0
+        us_cpu = (t_one - t_gram + t_gram * T / t_s) * 1e6
+        res["cpu_baseline"] = {"value": round(us_cpu, 1), "unit": "us/layer", "kind": "oracle",
+                               "cores": os.cpu_count(),
+                               "sample": f"the oracle on {t_s} of {T} tokens (numpy fp64, its "
+                                         "BLAS threads); the Gram part scaled to all tokens"}
+        log(f"cpu baseline: {res['cpu_baseline']}")
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -337,6 +441,11 @@ def main() -> int:
     ap.add_argument("--terms", type=int, default=0,
                     help="the layer with additive power-of-two factors of this many terms "
                          "(sa_shiftadd_gemm_terms) on the workload layer's shape")
+    ap.add_argument("--criterion", action="store_true",
+                    help="time the mixed-bit criterion of Eq. 3 for one layer (--shape N K, "
+                         "--tokens T)")
+    ap.add_argument("--tokens", type=int, default=262144,
+                    help="--criterion: calibration tokens (default 128 x 2048)")
     ap.add_argument("--quantize", action="store_true",
                     help="time the offline reparameterization (sa_quantize_bcq) instead")
     ap.add_argument("--shape", type=int, nargs=2, default=(4096, 4096), metavar=("N", "K"),
@@ -365,6 +474,8 @@ def main() -> int:
 
     if args.quantize:
         return bench_quantize(args)
+    if args.criterion:
+        return bench_criterion(args)
     if args.steps is None:
         args.steps = 4000
     if args.warmup is None:

@@ -266,7 +266,7 @@ SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch,
 
 /* H = X X^T (Eq. 3) on the matrix cores, fp32 accumulation of fp16 products.
  *   x  (device) fp16 bits [K][T] row-major (one row per input channel), 16-byte
- *      aligned; K % 64 == 0, T % 32 == 0 (pad with zero tokens; they add nothing).
+ *      aligned; K % 128 == 0, T % 32 == 0 (pad with zero tokens; they add nothing).
  *   H  (device) fp32 [K][K], fully overwritten (symmetric).
  * Asynchronous on `stream`. */
 SA_API int sa_gram_f16(const uint16_t *x, int K, int T, float *H, void *stream);

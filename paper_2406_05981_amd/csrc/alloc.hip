@@ -20,6 +20,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <type_traits>
 #include <vector>
 
 #include "shiftadd.h"
@@ -28,23 +29,26 @@ namespace {
 
 // ---------------------------------------------------------------- Gram matrix
 
-constexpr int kGT = 64;        // output tile: 64 x 64
-constexpr int kGK = 32;        // calibration columns per step
+constexpr int kGT = 128;       // output tile: 128 x 128
+constexpr int kGK = 32;        // calibration columns per stage
 constexpr int kGPad = kGK + 4; // LDS row stride in halves (72 bytes): spreads rows over banks
+constexpr int kGBuf = kGT * kGPad;
 
 typedef _Float16 half4 __attribute__((ext_vector_type(4)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 // Tile (ti, tj), ti >= tj, of H = X X^T for X fp16 [K][T] row-major.  Four
-// waves, each a 32 x 32 quarter (2 x 2 blocks of 16 x 16).  Per step the two
-// 64 x 32 slices of X are staged in LDS; one MFMA consumes 16 columns.
+// waves, each a 64 x 64 quarter (4 x 4 blocks of 16 x 16, 16 accumulators of
+// four floats).  The two 128 x 32 slices of X of a stage are double-buffered
+// in LDS; the next stage's slices are loaded into registers while the current
+// one is multiplied, so one barrier per stage suffices.
 // Operand layout of v_mfma_f32_16x16x16_f16: lane l holds row (l mod 16) of A
 // and column (l mod 16) of B at k = 4 (l / 16) .. 4 (l / 16) + 3; the result
 // holds rows 4 (l / 16) .. + 3 of column (l mod 16).
 __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x, int K, int T,
                                                   float* __restrict__ H) {
-    __shared__ uint16_t sa[kGT * kGPad];
-    __shared__ uint16_t sb[kGT * kGPad];
+    __shared__ uint16_t sa[2 * kGBuf];
+    __shared__ uint16_t sb[2 * kGBuf];
     // linear block index -> lower-triangular tile (ti >= tj)
     const int b = blockIdx.x;
     int ti = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
@@ -53,47 +57,72 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
     const int tj = b - ti * (ti + 1) / 2;
     const int i0 = ti * kGT, j0 = tj * kGT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;
-    // staging: thread -> (row, 8 halves)
+    const int wi = (wave >> 1) * 64, wj = (wave & 1) * 64;
+    // staging: thread -> rows lr and lr + 64, 8 halves at column lc
     const int lr = tid >> 2, lc = (tid & 3) * 8;
     const uint16_t* pa = x + (int64_t)(i0 + lr) * T + lc;
     const uint16_t* pb = x + (int64_t)(j0 + lr) * T + lc;
-    float4v acc[2][2];
+    const int64_t half = (int64_t)64 * T;
+    float4v acc[4][4];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int v = 0; v < 2; ++v) acc[u][v] = float4v{0.f, 0.f, 0.f, 0.f};
+        for (int v = 0; v < 4; ++v) acc[u][v] = float4v{0.f, 0.f, 0.f, 0.f};
     const int r16 = lane & 15, kq = (lane >> 4) * 4;
-    for (int t0 = 0; t0 < T; t0 += kGK) {
-        const uint4 va = *reinterpret_cast<const uint4*>(pa + t0);
-        const uint4 vb = *reinterpret_cast<const uint4*>(pb + t0);
-        __syncthreads();  // the previous step's reads are done
-        *reinterpret_cast<uint2*>(sa + lr * kGPad + lc) = make_uint2(va.x, va.y);
-        *reinterpret_cast<uint2*>(sa + lr * kGPad + lc + 4) = make_uint2(va.z, va.w);
-        *reinterpret_cast<uint2*>(sb + lr * kGPad + lc) = make_uint2(vb.x, vb.y);
-        *reinterpret_cast<uint2*>(sb + lr * kGPad + lc + 4) = make_uint2(vb.z, vb.w);
-        __syncthreads();
+
+    uint4 ra0 = *reinterpret_cast<const uint4*>(pa);
+    uint4 ra1 = *reinterpret_cast<const uint4*>(pa + half);
+    uint4 rb0 = *reinterpret_cast<const uint4*>(pb);
+    uint4 rb1 = *reinterpret_cast<const uint4*>(pb + half);
+    auto stage_store = [&](int buf) {
+        uint16_t* A = sa + buf * kGBuf;
+        uint16_t* Bm = sb + buf * kGBuf;
+        *reinterpret_cast<uint2*>(A + lr * kGPad + lc) = make_uint2(ra0.x, ra0.y);
+        *reinterpret_cast<uint2*>(A + lr * kGPad + lc + 4) = make_uint2(ra0.z, ra0.w);
+        *reinterpret_cast<uint2*>(A + (lr + 64) * kGPad + lc) = make_uint2(ra1.x, ra1.y);
+        *reinterpret_cast<uint2*>(A + (lr + 64) * kGPad + lc + 4) = make_uint2(ra1.z, ra1.w);
+        *reinterpret_cast<uint2*>(Bm + lr * kGPad + lc) = make_uint2(rb0.x, rb0.y);
+        *reinterpret_cast<uint2*>(Bm + lr * kGPad + lc + 4) = make_uint2(rb0.z, rb0.w);
+        *reinterpret_cast<uint2*>(Bm + (lr + 64) * kGPad + lc) = make_uint2(rb1.x, rb1.y);
+        *reinterpret_cast<uint2*>(Bm + (lr + 64) * kGPad + lc + 4) = make_uint2(rb1.z, rb1.w);
+    };
+    stage_store(0);
+    __syncthreads();
+    const int stages = T / kGK;
+    for (int st = 0; st < stages; ++st) {
+        const int buf = st & 1;
+        if (st + 1 < stages) {
+            const int t1 = (st + 1) * kGK;
+            ra0 = *reinterpret_cast<const uint4*>(pa + t1);
+            ra1 = *reinterpret_cast<const uint4*>(pa + half + t1);
+            rb0 = *reinterpret_cast<const uint4*>(pb + t1);
+            rb1 = *reinterpret_cast<const uint4*>(pb + half + t1);
+        }
+        const uint16_t* A = sa + buf * kGBuf;
+        const uint16_t* Bm = sb + buf * kGBuf;
 #pragma unroll
         for (int ks = 0; ks < kGK; ks += 16) {
-            half4 av[2], bv[2];
+            half4 av[4], bv[4];
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const uint2 ra = *reinterpret_cast<const uint2*>(sa + (wi + 16 * u + r16) * kGPad + ks + kq);
-                const uint2 rb = *reinterpret_cast<const uint2*>(sb + (wj + 16 * u + r16) * kGPad + ks + kq);
-                av[u] = __builtin_bit_cast(half4, ra);
-                bv[u] = __builtin_bit_cast(half4, rb);
+            for (int u = 0; u < 4; ++u) {
+                av[u] = __builtin_bit_cast(half4, *reinterpret_cast<const uint2*>(
+                                                      A + (wi + 16 * u + r16) * kGPad + ks + kq));
+                bv[u] = __builtin_bit_cast(half4, *reinterpret_cast<const uint2*>(
+                                                      Bm + (wj + 16 * u + r16) * kGPad + ks + kq));
             }
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-                for (int v = 0; v < 2; ++v)
+                for (int v = 0; v < 4; ++v)
                     acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x16f16(av[u], bv[v], acc[u][v], 0, 0, 0);
         }
+        if (st + 1 < stages) stage_store(buf ^ 1);
+        __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int v = 0; v < 2; ++v)
+        for (int v = 0; v < 4; ++v)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int i = i0 + wi + 16 * u + (lane >> 4) * 4 + e;
@@ -139,58 +168,90 @@ __global__ __launch_bounds__(256) void k_reverse(const float* __restrict__ H, in
 constexpr int kNB = 64;             // panel width
 constexpr int kNBP = kNB + 1;       // LDS row stride (doubles)
 
-// Diagonal block [j, j + 64) factored in place (unblocked, right-looking).  A
-// non-positive pivot gives NaN, which then runs through every later value.
-__global__ __launch_bounds__(256) void k_chol_diag(double* __restrict__ A, int K, int j) {
-    __shared__ double a[kNB * kNBP];
-    const int nb = min(kNB, K - j);
-    for (int e = threadIdx.x; e < nb * nb; e += 256) {
-        const int r = e / nb, c = e % nb;
-        a[r * kNBP + c] = c <= r ? A[(int64_t)(j + r) * K + j + c] : 0.0;
-    }
-    __syncthreads();
-    for (int c = 0; c < nb; ++c) {
-        if (threadIdx.x == 0) a[c * kNBP + c] = sqrt(a[c * kNBP + c]);
-        __syncthreads();
-        const double p = a[c * kNBP + c];
-        for (int r = c + 1 + threadIdx.x; r < nb; r += 256) a[r * kNBP + c] /= p;
-        __syncthreads();
-        const int m = nb - c - 1;  // trailing lower triangle, m (m + 1) / 2 entries
-        for (int e = threadIdx.x; e < m * m; e += 256) {
-            const int r = c + 1 + e / m, s = c + 1 + e % m;
-            if (s <= r) a[r * kNBP + s] -= a[r * kNBP + c] * a[s * kNBP + c];
-        }
-        __syncthreads();
-    }
-    for (int e = threadIdx.x; e < nb * nb; e += 256) {
-        const int r = e / nb, c = e % nb;
-        if (c <= r) A[(int64_t)(j + r) * K + j + c] = a[r * kNBP + c];
+// Diagonal block [j, j + 64) factored in place by one wave, Crout order: lane r
+// holds row r of the block in registers (64 doubles); for column c, lane c
+// finishes its diagonal entry and every lane below it its entry of column c,
+// each a dot product with row c, whose entries are broadcast from lane c
+// (readlane).  A non-positive pivot gives NaN, which then runs through every
+// later value.
+template <int C>
+__device__ inline double lane_value(double v) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, C);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), C);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+template <int B, int E, typename F>
+__device__ inline void cfor(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        cfor<B + 1, E>(f);
     }
 }
 
-// Panel below the diagonal block: row r (r >= j + 64) solves x L11^T = a.  One
-// thread per row; L11 and the 64 rows of the workgroup staged in LDS.
+__global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K, int j) {
+    const int r = threadIdx.x;
+    const int nb = min(kNB, K - j);
+    double a[kNB];
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        a[c] = (r < nb && c < nb && c <= r) ? A[(int64_t)(j + r) * K + j + c] : (c == r ? 1.0 : 0.0);
+    });
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        // row c's finished entries 0..c-1, from lane c
+        double rc[c > 0 ? c : 1];
+        cfor<0, c>([&](auto k_) {
+            constexpr int k = decltype(k_)::value;
+            rc[k] = lane_value<c>(a[k]);
+        });
+        double v = a[c];
+        cfor<0, c>([&](auto k_) {
+            constexpr int k = decltype(k_)::value;
+            v = fma(-a[k], rc[k], v);
+        });
+        // lane c: the pivot; lanes below: divide by it
+        const double piv = lane_value<c>(r == c ? sqrt(v) : 0.0);
+        if (r == c) a[c] = piv;
+        else if (r > c) a[c] = v / piv;
+    });
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        if (r < nb && c < nb && c <= r) A[(int64_t)(j + r) * K + j + c] = a[c];
+    });
+}
+
+// Panel below the diagonal block: row r (r >= j + 64) solves x L11^T = a, one
+// row per lane held in registers, L11 in LDS (every lane reads the same entry:
+// a broadcast).
 __global__ __launch_bounds__(64) void k_chol_trsm(double* __restrict__ A, int K, int j) {
-    __shared__ double l11[kNB * kNBP];
-    __shared__ double rows[kNB * kNBP];
-    const int r0 = j + kNB + blockIdx.x * kNB;
+    __shared__ double l11[kNB * kNB];
     for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
-        const int r = e / kNB, c = e % kNB;
-        l11[r * kNBP + c] = c <= r ? A[(int64_t)(j + r) * K + j + c] : 0.0;
-        rows[r * kNBP + c] = r0 + r < K ? A[(int64_t)(r0 + r) * K + j + c] : 0.0;
+        const int rr = e / kNB, c = e % kNB;
+        l11[e] = c <= rr ? A[(int64_t)(j + rr) * K + j + c] : 0.0;
     }
     __syncthreads();
-    double* xr = rows + threadIdx.x * kNBP;
-    for (int c = 0; c < kNB; ++c) {
-        double v = xr[c];
-        for (int k = 0; k < c; ++k) v -= xr[k] * l11[c * kNBP + k];
-        xr[c] = v / l11[c * kNBP + c];
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
-        const int r = e / kNB, c = e % kNB;
-        if (r0 + r < K) A[(int64_t)(r0 + r) * K + j + c] = rows[r * kNBP + c];
-    }
+    const int row = j + kNB + blockIdx.x * 64 + threadIdx.x;
+    const bool ok = row < K;
+    double x[kNB];
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        x[c] = ok ? A[(int64_t)row * K + j + c] : 0.0;
+    });
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        double v = x[c];
+        cfor<0, c>([&](auto k_) {
+            constexpr int k = decltype(k_)::value;
+            v = fma(-x[k], l11[c * kNB + k], v);
+        });
+        x[c] = v / l11[c * kNB + c];
+    });
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        if (ok) A[(int64_t)row * K + j + c] = x[c];
+    });
 }
 
 // Trailing update of the lower triangle: A[r][s] -= sum_c L[r][c] L[s][c] over
@@ -348,11 +409,11 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
     const int grid = (int)(((n + 255) / 256) < 8192 ? (n + 255) / 256 : 8192);
     hipLaunchKernelGGL(k_reverse, dim3(grid), dim3(256), 0, s, H, K, lambda, A);
     for (int j = 0; j < K; j += kNB) {
-        hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(256), 0, s, A, K, j);
+        hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(64), 0, s, A, K, j);
         const int below = K - j - kNB;
         if (below > 0) {
             const int rb = (below + kNB - 1) / kNB;
-            hipLaunchKernelGGL(k_chol_trsm, dim3(rb), dim3(64), 0, s, A, K, j);
+            hipLaunchKernelGGL(k_chol_trsm, dim3((below + 63) / 64), dim3(64), 0, s, A, K, j);
             hipLaunchKernelGGL(k_chol_syrk, dim3(rb * (rb + 1) / 2), dim3(256), 0, s, A, K, j);
         }
     }

@@ -258,10 +258,10 @@ def test_quantize_terms_validation_codes():
 
 def test_alloc_validation_codes():
     L = sa.lib
-    assert L.sa_gram_f16(None, 64, 32, A, None) == sa.SA_ERR_NULL
-    assert L.sa_gram_f16(A, 100, 32, A, None) == sa.SA_ERR_SHAPE     # K % 64
-    assert L.sa_gram_f16(A, 64, 40, A, None) == sa.SA_ERR_SHAPE      # T % 32
-    assert L.sa_gram_f16(A + 8, 64, 32, A, None) == sa.SA_ERR_ALIGN
+    assert L.sa_gram_f16(None, 128, 32, A, None) == sa.SA_ERR_NULL
+    assert L.sa_gram_f16(A, 192, 32, A, None) == sa.SA_ERR_SHAPE     # K % 128
+    assert L.sa_gram_f16(A, 128, 40, A, None) == sa.SA_ERR_SHAPE     # T % 32
+    assert L.sa_gram_f16(A + 8, 128, 32, A, None) == sa.SA_ERR_ALIGN
     ws = L.sa_inverse_cholesky_workspace(64)
     assert ws >= 64 * 64 * 8
     assert L.sa_inverse_cholesky_diag(A, 64, 0.01, A, None, ws, None) == sa.SA_ERR_NULL

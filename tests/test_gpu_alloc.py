@@ -57,7 +57,7 @@ def gpu_d(H, damp):
     return d.cpu().numpy()
 
 
-@pytest.mark.parametrize("K,T", [(64, 32), (128, 96), (256, 512), (512, 2048)])
+@pytest.mark.parametrize("K,T", [(128, 32), (128, 96), (256, 512), (512, 2048), (1024, 160)])
 def test_gram(K, T):
     say(f"gram K={K} T={T}")
     x = calib(K, T, seed=K + T)
