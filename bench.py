@@ -111,7 +111,7 @@ def cpu_baseline(d: dict, bytes_step: int, seconds: float) -> dict:
     sample = (f"{'all' if sel is None else rows} of {N} output rows x batch {d['B']}, "
               f"median of {len(times)} runs, fp64 oracle, OpenMP")
     return {"value": bytes_step / us_layer / 1e3, "unit": "GB/s", "cores": used, "kind": "oracle",
-            "sample": sample, "us_per_layer": us_layer}
+            "sample": sample, "us_per_layer": us_layer, **host_info()}
 
 
 def time_read_floor(sa, nbytes: int, rotate_mb: float, steps: int, stream) -> dict:
@@ -213,6 +213,122 @@ def cpu_baseline_quant(w, q: int, G: int, T: int, seconds: float) -> dict:
     return {"value": round(us_layer, 1), "unit": "us/layer", "cores": 1, "kind": "oracle",
             "sample": f"first {rows} of {N} rows, median of {len(times)} runs, fp64 numpy "
                       "oracle (one thread), scaled to the whole layer"}
+
+
+def device_info() -> dict:
+    import torch
+
+    p = torch.cuda.get_device_properties(0)
+    return {"name": p.name, "gcn_arch": getattr(p, "gcnArchName", None),
+            "compute_units": p.multi_processor_count, "total_memory_gb": round(p.total_memory / 2**30, 1)}
+
+
+def host_info() -> dict:
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
+
+
+def bench_layer_set(args) -> int:
+    """The LLaMA-2-7B decoder layer set: the 7 projections (q, k, v, o 4096^2;
+    up, gate 11008x4096; down 4096x11008; q per layer from {2, 3, 4} with mean 3)
+    replicated over 32 decoder layers with distinct seeds (about 2.6 GB of
+    planes, which no cache holds), run back to back; one step = the 224 layers.
+    Tokens/s counts these linear layers only (no attention, no norms)."""
+    import numpy as np
+    import torch
+
+    import workloads
+    import paper_2406_05981_amd.shiftadd as sa
+
+    w = workloads.workload("llama2_7b_layer_set")
+    batches = list(w.batches)
+    steps = args.steps if args.steps is not None else 200
+    warmup = args.warmup if args.warmup is not None else 20
+    t0 = time.perf_counter()
+    layers = []
+    total_bytes = {B: 0 for B in batches}
+    for d in range(w.depth):
+        for li, L in enumerate(w.layers):
+            c = workloads.layer_coins_batches(w.key, li, batches, copy=d)
+            coins = torch.from_numpy(c["coins"]).cuda()
+            shifts = torch.arange(8, device="cuda", dtype=torch.uint8)
+            bits = (coins.unsqueeze(-1) >> shifts) & 1            # little-endian bits
+            signs = (bits.to(torch.int8) * 2 - 1).reshape(L.q, L.N, L.K)
+            packed = sa.pack_weights(signs)
+            del coins, bits, signs
+            xs = {B: torch.from_numpy(c["x"][B]).cuda() for B in batches}
+            ys = {B: torch.empty((B, L.N), dtype=torch.float32, device="cuda") for B in batches}
+            layers.append((L, packed, torch.from_numpy(c["exps"]).cuda(), xs, ys))
+            for B in batches:
+                total_bytes[B] += algorithmic_bytes(L.q, L.N, L.K, w.group, B)
+    torch.cuda.synchronize()
+    log(f"layer set: {len(layers)} layers generated and packed in {time.perf_counter() - t0:.1f} s")
+    stream = torch.cuda.Stream()
+    res_b = {}
+    for B in batches:
+        def step():
+            for (L, packed, exps, xs, ys) in layers:
+                sa.sa_shiftadd_gemm(xs[B], packed, exps, L.q, L.N, L.K, w.group, B, ys[B])
+
+        with torch.cuda.stream(stream):
+            step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            step()
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            for _ in range(steps):
+                g.replay()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        gbs = total_bytes[B] / us / 1e3
+        res_b[str(B)] = {"us_per_step": round(us, 2), "tokens_per_s": round(B * 1e6 / us, 1),
+                         "GB_per_s": round(gbs, 1), "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                         "bytes_per_step": total_bytes[B]}
+        log(f"B={B}: {us:.1f} us per 224 layers, {B * 1e6 / us:.1f} tokens/s, {gbs:.1f} GB/s")
+        del g
+    B0 = args.batch or 1
+    r0 = res_b[str(B0)]
+    out = {
+        "metric": "tokens/s of the LLaMA-2-7B decoder linear layers (7 projections x 32 layers)",
+        "value": r0["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": r0["us_per_step"] / 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Bernoulli(0.5) planes, uniform int8 exponents in [-10,-3], "
+                "N(0,1) fp16 activations with 1% outlier channels x20); linear layers only",
+        "config": {"workload": w.key, "batch": B0, "layers": [f"{L.name} {L.N}x{L.K} q={L.q}"
+                                                              for L in w.layers],
+                   "depth": w.depth, "group": w.group, "launch": "hip graph replay"},
+        "per_batch": res_b,
+        "roofline": {"bound": "hbm", "achieved": r0["GB_per_s"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(r0["GB_per_s"] / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+        "device": device_info(),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def bench_quantize(args) -> int:
@@ -441,6 +557,9 @@ def main() -> int:
     ap.add_argument("--terms", type=int, default=0,
                     help="the layer with additive power-of-two factors of this many terms "
                          "(sa_shiftadd_gemm_terms) on the workload layer's shape")
+    ap.add_argument("--layer-set", action="store_true",
+                    help="time the LLaMA-2-7B decoder layer set (7 projections x 32 layers) at "
+                         "batch 1, 4, 8, 16; tokens/s at --batch (default 1)")
     ap.add_argument("--criterion", action="store_true",
                     help="time the mixed-bit criterion of Eq. 3 for one layer (--shape N K, "
                          "--tokens T)")
@@ -476,6 +595,8 @@ def main() -> int:
         return bench_quantize(args)
     if args.criterion:
         return bench_criterion(args)
+    if args.layer_set:
+        return bench_layer_set(args)
     if args.steps is None:
         args.steps = 4000
     if args.warmup is None:
@@ -666,6 +787,10 @@ def main() -> int:
             "traffic": traffic,
         },
     }
+    out["device"] = device_info()
+    out["input_sha256"] = {k: workloads.sha256(v)[:16] for k, v in
+                           (("signs", d0["signs"]), ("x", d0["x"]),
+                            ("exps", d0.get("exps", d0.get("col_exps", d0.get("blk_exps")))))}
     if read_floor is not None:
         out["read_floor"] = read_floor
         out["frac_of_read_floor"] = round(read_floor["us_per_layer"] / us_layer, 4)

@@ -52,6 +52,7 @@ __all__ = [
     "colwise_case",
     "blockwise_case",
     "terms_case",
+    "layer_coins_batches",
 ]
 
 
@@ -314,3 +315,24 @@ def terms_case(q: int, N: int, K: int, G: int, B: int, T: int, seed: int = 0,
     return dict(signs=signs, exps=exps, term_signs=tsg, x=x16, outlier_channels=idx, q=q, N=N,
                 K=K, G=G, B=B, T=T, name=f"terms(q={q},N={N},K={K},G={G},B={B},T={T})",
                 seed=seed, copy=copy)
+
+
+def layer_coins_batches(key: str, layer: int, batches: Sequence[int], seed: int = 0,
+                        copy: int = 0) -> dict:
+    """``layer_inputs_batches`` without the unpacking of the sign bits: the same
+    draws, with the planes as the drawn bytes (``coins`` uint8 [q][N][K/8]; bit
+    j of byte c, little-endian, is the coin of column 8c+j, 1 -> +1).  For
+    benchmarks that unpack on the device."""
+    w = WORKLOADS[key]
+    L = w.layers[layer]
+    rng = np.random.default_rng(np.random.SeedSequence([seed, w.config_id, layer + 1000 * copy]))
+    coins = rng.integers(0, 256, size=(L.q, L.N, L.K // 8), dtype=np.uint8)
+    exps = rng.integers(w.exp_range[0], w.exp_range[1] + 1, size=(L.q, L.N, L.K // w.group),
+                        dtype=np.int8)
+    state = rng.bit_generator.state
+    xs = {}
+    for B in batches:
+        rng.bit_generator.state = state
+        xs[B] = _draw_x(rng, L.K, B, w.outlier_fraction, w.outlier_scale)[0]
+    return dict(coins=coins, exps=exps, x=xs, q=L.q, N=L.N, K=L.K, G=w.group,
+                name=f"{key}/{L.name}", seed=seed, copy=copy)
