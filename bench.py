@@ -51,8 +51,11 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+# the dominant kernel of each launch path; the additive layer ("add") runs the
+# row kernel (path 1) or the batch kernel (path 2) in its additive mode
 KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col",
-           4: "k_gemm_rows_blk", 5: "k_gemm_rows_add"}
+           4: "k_gemm_rows_blk", 5: "k_gemm_batch_blk", "add1": "k_gemm_rows_add",
+           "add2": "k_gemm_batch_add"}
 
 
 def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
@@ -623,7 +626,8 @@ def main() -> int:
         # T exponent bytes and T term-sign bytes per (plane, row, group)
         bytes_step = algorithmic_bytes(q, N, K, G, B) + (2 * terms - 1) * q * N * (K // G)
         weight_bytes = q * N * K // 8 + 2 * terms * q * N * (K // G)
-        plan = dict(sa.sa_plan_gemm(q, N, K, G, 1), path=5)
+        plan = sa.sa_plan_gemm(q, N, K, G, B)
+        plan = dict(plan, path=f"add{plan['path']}")
     elif blockwise:
         bytes_step = algorithmic_bytes(q, N, K, K, B) - q * N + q * nb * (K // 8)
         weight_bytes = q * N * K // 8 + q * nb * (K // 8)

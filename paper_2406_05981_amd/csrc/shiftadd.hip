@@ -755,11 +755,15 @@ constexpr int kBatchRows = 64;                                    // most rows p
 struct BatchArgs {
     const uint16_t* x;  // activations [B][K]
     const uint8_t* packed;
-    const int8_t* exps;
+    const int8_t* exps;        // row-wise [q][N][K/G]; additive [q][N][K/G][T]
     int q, N, K, G, B;
     float* y;     // [B][N]
     int n_tiles;  // row tiles of 16*KW rows
     int n_quads;  // ceil(B / 4)
+    const int8_t* term_signs;  // additive: [q][N][K/G][T]
+    int terms;                 // additive: T
+    const int8_t* blk_exps;    // block-wise: [q][NB][K/8]
+    int row_block, NB;         // block-wise
 };
 
 // One piece for this lane: KW key words of Q planes, their exponents, and the
@@ -769,6 +773,8 @@ struct BatchJob {
     uint32_t w[Q][KW];
     int e[Q];
     uint4 xr;
+    uint32_t et[Q], st[Q];  // additive: T exponent bytes, T term signs
+    uint4 eb[Q];            // block-wise: the 16 exponents of the block in the row's block of rows
 };
 
 template <int KW>
@@ -791,9 +797,13 @@ __device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
     asm volatile("" : "+v"(j.e[i]));
 }
 
-template <int Q, int KW>
+// MODE: kRowWise, kAdditive (each plane's group sums shifted by T signed terms)
+// or kBlockWise (each queried entry shifted by its key's exponent).
+template <int Q, int KW, int MODE>
 __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
     constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
+    constexpr bool ADD = MODE == kAdditive;
+    constexpr bool BLK = MODE == kBlockWise;
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4;
@@ -835,9 +845,25 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 
     auto load_job = [&](int pc, BatchJob<Q, KW>& j) {
         const int J = imin(kRowWaves * pc + wave, C16 - 1);
-        const int8_t* e = exp_row + (bpg == 1 ? J : J / bpg);
+        if constexpr (ADD) {
+            const int64_t off = ((int64_t)n * NG + (bpg == 1 ? J : J / bpg)) * a.terms;
+            const int64_t plane = (int64_t)a.N * NG * a.terms;
 #pragma unroll
-        for (int i = 0; i < Q; ++i) j.e[i] = e[(int64_t)i * a.N * NG];
+            for (int i = 0; i < Q; ++i) {
+                j.et[i] = load_terms(a.exps + i * plane + off, a.terms);
+                j.st[i] = load_terms(a.term_signs + i * plane + off, a.terms);
+            }
+        } else if constexpr (BLK) {
+            const int rb = n / a.row_block;
+#pragma unroll
+            for (int i = 0; i < Q; ++i)
+                j.eb[i] = *reinterpret_cast<const uint4*>(a.blk_exps +
+                                                          ((int64_t)i * a.NB + rb) * C + 16 * J);
+        } else {
+            const int8_t* e = exp_row + (bpg == 1 ? J : J / bpg);
+#pragma unroll
+            for (int i = 0; i < Q; ++i) j.e[i] = e[(int64_t)i * a.N * NG];
+        }
         j.xr = *reinterpret_cast<const uint4*>(a.x + (int64_t)bx * a.K +
                                                8 * (kBlockChunks * J + bc));
         const uint8_t* kp = key_row + (int64_t)kBlockChunks * J * R;
@@ -876,6 +902,18 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
             __builtin_amdgcn_sched_barrier(0);
             pin_batch_plane<Q, KW>(j, i);
             float s[kQuad];
+            // block-wise: the exponents of this lane's KW key words (4 keys each),
+            // rotated to the row's key order
+            uint32_t ekw[KW];
+            if constexpr (BLK) {
+                uint32_t ek[4];
+                rotate16(j.eb[i], rr, ek);
+#pragma unroll
+                for (int k = 0; k < KW; ++k) {
+                    const int wsel = KW * dsl + k;
+                    ekw[k] = wsel == 0 ? ek[0] : wsel == 1 ? ek[1] : wsel == 2 ? ek[2] : ek[3];
+                }
+            }
 #pragma unroll
             for (int k = 0; k < KW; ++k) {
                 // one key word at a time: its 8 loads go out together, then
@@ -895,7 +933,18 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    if (k == 0 && t == 0) {
+                    if constexpr (BLK) {
+                        const int ex = (int)(int8_t)(ekw[k] >> (8 * t));
+                        const float v0 = ldexpf(L[t].x + H[t].x, ex);
+                        const float v1 = ldexpf(L[t].y + H[t].y, ex);
+                        const float v2 = ldexpf(L[t].z + H[t].z, ex);
+                        const float v3 = ldexpf(L[t].w + H[t].w, ex);
+                        if (k == 0 && t == 0) {
+                            s[0] = v0; s[1] = v1; s[2] = v2; s[3] = v3;
+                        } else {
+                            s[0] += v0; s[1] += v1; s[2] += v2; s[3] += v3;
+                        }
+                    } else if (k == 0 && t == 0) {
                         s[0] = L[0].x + H[0].x;
                         s[1] = L[0].y + H[0].y;
                         s[2] = L[0].z + H[0].z;
@@ -910,8 +959,27 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                 // the word's adds complete here, so its loads' registers free up
                 asm volatile("" : "+v"(s[0]), "+v"(s[1]), "+v"(s[2]), "+v"(s[3]));
             }
+            if constexpr (BLK) {
 #pragma unroll
-            for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
+                for (int u = 0; u < kQuad; ++u) tot[u] += s[u] * keep;
+            } else if constexpr (ADD) {
+                asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
+#pragma unroll
+                for (int tt = 0; tt < kMaxTerms; ++tt) {
+                    const int sg = (int)(int8_t)(j.st[i] >> (8 * tt));
+                    if (tt < a.terms && sg != 0) {
+                        const int ex = (int)(int8_t)(j.et[i] >> (8 * tt));
+#pragma unroll
+                        for (int u = 0; u < kQuad; ++u) {
+                            const float v = ldexpf(s[u], ex) * keep;
+                            tot[u] += sg < 0 ? -v : v;
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
+            }
         }
     };
 
@@ -953,19 +1021,19 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     }
 }
 
-template <int Q, int KW>
+template <int Q, int KW, int MODE = kRowWise>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_batch(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];  // 64 KB
     __shared__ float4 red[kRowWaves * kBatchRows];            // 8 KB
-    gemm_batch_body<Q, KW>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
 }
 
-template <int Q, int KW>
+template <int Q, int KW, int MODE = kRowWise>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_batch_wide(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];
     __shared__ float4 red[kRowWaves * kBatchRows];
-    gemm_batch_body<Q, KW>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
 }
 
 // ---------------------------------------------------------------- read probe
@@ -1108,11 +1176,11 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
     p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
-// Block-wise factors: the row kernel with a shift per key (path 4).
+// Block-wise factors: the row kernel (batch 1, path 4) or the batch kernel
+// (batch >= 2, path 5) with a shift per key.
 void make_plan_blockwise(int q, int N, int K, int batch, sa_plan* p) {
-    make_plan(q, N, K, 128, 1, p);  // the row kernel's geometry
-    (void)batch;
-    p->path = 4;
+    make_plan(q, N, K, 128, batch, p);
+    p->path = batch >= 2 ? 5 : 4;
 }
 
 int launch_status() { return hipGetLastError() == hipSuccess ? SA_OK : SA_ERR_HIP; }
@@ -1138,25 +1206,26 @@ void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
     }
 }
 
-template <int KW>
+template <int KW, int MODE>
 void launch_batch_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
     const dim3 g(workgroups), b(kRowThreads);
     switch (q) {
-        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW>), g, b, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW>), g, b, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW>), g, b, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW>), g, b, 0, s, a); break;
-        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW>), g, b, 0, s, a); break;
-        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW>), g, b, 0, s, a); break;
-        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW>), g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW>), g, b, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE>), g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE>), g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW, MODE>), g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW, MODE>), g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW, MODE>), g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW, MODE>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW, MODE>), g, b, 0, s, a); break;
     }
 }
 
+template <int MODE = kRowWise>
 void launch_batch(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t s) {
-    if (kw == 4) launch_batch_kw<4>(q, a, workgroups, s);
-    else if (kw == 2) launch_batch_kw<2>(q, a, workgroups, s);
-    else launch_batch_kw<1>(q, a, workgroups, s);
+    if (kw == 4) launch_batch_kw<4, MODE>(q, a, workgroups, s);
+    else if (kw == 2) launch_batch_kw<2, MODE>(q, a, workgroups, s);
+    else launch_batch_kw<1, MODE>(q, a, workgroups, s);
 }
 
 }  // namespace
@@ -1284,6 +1353,27 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
         return SA_ERR_ALIGN;
     sa_plan plan;
     make_plan_blockwise(q, N, K, batch, &plan);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (plan.path == 5) {
+        BatchArgs a{};
+        a.x = x;
+        a.packed = packed_bits;
+        a.exps = blk_exps;  // not read in this mode
+        a.blk_exps = blk_exps;
+        a.q = q;
+        a.N = N;
+        a.K = K;
+        a.G = K;
+        a.B = batch;
+        a.y = y;
+        a.row_block = row_block;
+        a.NB = (N + row_block - 1) / row_block;
+        const int kw = plan.rows_per_wg / 16;
+        a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
+        a.n_quads = (batch + kQuad - 1) / kQuad;
+        launch_batch<kBlockWise>(q, kw, a, plan.workgroups, s);
+        return launch_status();
+    }
     RowsArgs a{};
     a.x = x;
     a.packed = packed_bits;
@@ -1298,7 +1388,6 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
     a.row_block = row_block;
     a.NB = (N + row_block - 1) / row_block;
     const dim3 g(plan.workgroups), b(kRowThreads);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows_blk<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows_blk<2>, g, b, 0, s, a); break;
@@ -1326,7 +1415,27 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
     if ((reinterpret_cast<uintptr_t>(exps) & al) || (reinterpret_cast<uintptr_t>(term_signs) & al))
         return SA_ERR_ALIGN;
     sa_plan plan;
-    make_plan(q, N, K, group, 1, &plan);  // the row kernel's geometry
+    make_plan(q, N, K, group, batch, &plan);  // row kernel (batch 1) or batch kernel
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (plan.path == 2) {
+        BatchArgs a{};
+        a.x = x;
+        a.packed = packed_bits;
+        a.exps = exps;
+        a.term_signs = term_signs;
+        a.terms = terms;
+        a.q = q;
+        a.N = N;
+        a.K = K;
+        a.G = group;
+        a.B = batch;
+        a.y = y;
+        const int kw = plan.rows_per_wg / 16;
+        a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
+        a.n_quads = (batch + kQuad - 1) / kQuad;
+        launch_batch<kAdditive>(q, kw, a, plan.workgroups, s);
+        return launch_status();
+    }
     RowsArgs a{};
     a.x = x;
     a.packed = packed_bits;
@@ -1341,7 +1450,6 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
     const dim3 g(plan.workgroups), b(kRowThreads);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows_add<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows_add<2>, g, b, 0, s, a); break;

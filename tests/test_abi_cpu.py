@@ -220,6 +220,8 @@ def test_blockwise_validation_codes():
     assert call(y=A + 4) == sa.SA_ERR_ALIGN
     p = sa.sa_plan_gemm_blockwise(3, 4096, 4096, 512, 1)
     assert p["path"] == 4 and p["workgroups"] == 256
+    p = sa.sa_plan_gemm_blockwise(3, 4096, 4096, 512, 16)  # the batch kernel
+    assert p["path"] == 5 and p["rows_per_wg"] == 64 and p["workgroups"] == 256
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm_blockwise(3, 4096, 4096, 0, 1)
 

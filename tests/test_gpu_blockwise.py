@@ -131,3 +131,58 @@ def test_blockwise_error_codes():
     with pytest.raises(sa.SaError):
         sa.sa_shiftadd_gemm_blockwise(dev(c["x"]), packed, dev(c["blk_exps"]), 2, 64, 256, 0, 1,
                                       y)
+
+
+# Batch >= 2 runs the batch kernel (plan path 5): 16, 32 or 64 rows per
+# workgroup (KW = 1, 2, 4 key words per lane) and four batch rows per table.
+BATCH_CASES = [
+    # (q, N, K, B, row_block, label)
+    (3, 1000, 1024, 8, 125, "KW=1, two quads"),
+    (3, 4096, 1024, 8, 512, "KW=2"),
+    (4, 4096, 512, 16, 512, "KW=4, four planes"),
+    (8, 2048, 512, 16, 256, "KW=2, eight planes"),
+    (2, 130, 384, 5, 17, "ragged quad and rows, 17-row blocks"),
+    (1, 77, 4224, 6, 1, "a factor per row, ragged last piece"),
+    (5, 300, 2048, 13, 40, "five planes, two pieces, ragged quad"),
+]
+
+
+@pytest.mark.parametrize("q,N,K,B,rb,label", BATCH_CASES, ids=[c[-1] for c in BATCH_CASES])
+def test_blockwise_batch_parity(q, N, K, B, rb, label):
+    plan = sa.sa_plan_gemm_blockwise(q, N, K, rb, B)
+    assert plan["path"] == 5
+    say(f"blockwise batch q={q} N={N} K={K} B={B} row_block={rb} "
+        f"rows/wg={plan['rows_per_wg']}: {label}")
+    c = workloads.blockwise_case(q, N, K, B, rb, seed=q + N + K + B + rb)
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_blockwise(c["x"], c["signs"], c["blk_exps"], rb)
+    check(y, y_ref, a_ref, label)
+
+
+def test_blockwise_batch_rows_agree_with_batch_one():
+    """Each batch row of the batch kernel against the row kernel on that row
+    alone (another kernel), within the bar of both against the oracle."""
+    q, N, K, B, rb = 3, 1024, 2048, 8, 128
+    c = workloads.blockwise_case(q, N, K, B, rb, seed=5)
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_blockwise(c["x"], c["signs"], c["blk_exps"], rb)
+    check(y, y_ref, a_ref, "batch 8")
+    for b in (0, 5, 7):
+        one = dict(c, B=1, x=c["x"][b:b + 1])
+        y1 = run(one)
+        check(y1, y_ref[b:b + 1], a_ref[b:b + 1], f"batch row {b} alone")
+
+
+@pytest.mark.parametrize("N,K", [(4096, 4096), (11008, 4096)])
+def test_blockwise_batch_full_size_sampled(N, K):
+    """LLaMA-2-7B projection shapes, q = 3, batch 16, row_block = N / 8; 256
+    sampled rows."""
+    q, B, rb = 3, 16, N // 8
+    say(f"blockwise batch full size N={N} K={K} B={B}")
+    c = workloads.blockwise_case(q, N, K, B, rb, seed=2)
+    y = run(c)
+    rows = np.sort(np.random.default_rng(1).choice(N, 256, replace=False))
+    rows[-1] = N - 1
+    y_ref, a_ref = oracle.shiftadd_gemm_blockwise(c["x"], c["signs"], c["blk_exps"], rb,
+                                                  rows=rows)
+    check(y[:, rows], y_ref, a_ref, f"{N}x{K} batch {B} sampled")

@@ -92,3 +92,51 @@ def test_terms_full_size_sampled():
     y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G,
                                               rows=rows)
     check(y[:, rows], y_ref, a_ref, "4096x4096 sampled")
+
+
+# Batch >= 2 runs the batch kernel: 16, 32 or 64 rows per workgroup and four
+# batch rows per table.
+BATCH_CASES = [
+    # (q, N, K, G, B, T, label)
+    (3, 1000, 1024, 128, 8, 2, "KW=1, two quads"),
+    (3, 4096, 1024, 256, 8, 3, "KW=2, G = 256, three terms"),
+    (4, 4096, 512, 128, 16, 4, "KW=4, four terms"),
+    (8, 2048, 512, 512, 16, 2, "KW=2, eight planes, G = K"),
+    (2, 130, 384, 384, 5, 3, "ragged quad and rows"),
+    (1, 77, 4224, 128, 6, 4, "ragged last piece"),
+    (5, 300, 2048, 1024, 13, 2, "five planes, two pieces, ragged quad"),
+]
+
+
+@pytest.mark.parametrize("q,N,K,G,B,T,label", BATCH_CASES, ids=[c[-1] for c in BATCH_CASES])
+def test_terms_batch_parity(q, N, K, G, B, T, label):
+    assert sa.sa_plan_gemm(q, N, K, G, B)["path"] == 2
+    say(f"terms batch q={q} N={N} K={K} G={G} B={B} T={T}: {label}")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=q + N + K + B + T)
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G)
+    check(y, y_ref, a_ref, label)
+
+
+def test_one_term_batch_matches_row_wise_batch_kernel():
+    q, N, K, G, B = 3, 2048, 2048, 128, 8
+    c = workloads.terms_case(q, N, K, G, B, 1, seed=12)
+    assert (c["term_signs"] != 0).all()
+    y = run(c)
+    yr = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"][..., 0]), q,
+                        N, K, G, B, yr)
+    torch.cuda.synchronize()
+    assert np.array_equal(y, yr.cpu().numpy().astype(np.float64))  # same arithmetic
+
+
+def test_terms_batch_full_size_sampled():
+    q, N, K, G, B, T = 3, 4096, 4096, 128, 16, 2
+    say("terms batch full size 4096x4096 B=16 T=2")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=2)
+    y = run(c)
+    rows = np.sort(np.random.default_rng(1).choice(N, 256, replace=False))
+    rows[-1] = N - 1
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G,
+                                              rows=rows)
+    check(y[:, rows], y_ref, a_ref, "4096x4096 batch 16 sampled")
