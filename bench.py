@@ -54,7 +54,7 @@ def source_hash() -> str:
 # the dominant kernel of each launch path; the additive layer ("add") runs the
 # row kernel (path 1) or the batch kernel (path 2) in its additive mode
 KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col",
-           4: "k_gemm_rows_blk", 5: "k_gemm_batch_blk", "add1": "k_gemm_rows_add",
+           4: "k_gemm_rows_blk", 5: "k_gemm_batch_blk", 6: "k_gemm_batch_col", "add1": "k_gemm_rows_add",
            "add2": "k_gemm_batch_add"}
 
 

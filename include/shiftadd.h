@@ -180,9 +180,10 @@ SA_API int sa_quantize_bcq_terms(const float *w, int N, int K, int q, int group,
 typedef struct {
     int path;         /* 0: generic kernel (any group); group % 128 == 0: 1 row kernel
                          (batch 1), 2 batch kernel (batch >= 2); 3: the row kernel
-                         with column-wise factors (sa_shiftadd_gemm_colwise); 4: the
+                         with column-wise factors (sa_shiftadd_gemm_colwise, batch 1); 4: the
                          row kernel with block-wise factors (sa_shiftadd_gemm_blockwise,
-                         batch 1), 5 the batch kernel with block-wise factors (batch >= 2) */
+                         batch 1), 5 the batch kernel with block-wise factors (batch >= 2);
+                         6 the batch kernel with column-wise factors (batch >= 2) */
     int rows_per_wg;  /* output rows per workgroup (the largest share when the
                          row kernel spreads row groups unevenly) */
     int workgroups;   /* workgroups of the launch */

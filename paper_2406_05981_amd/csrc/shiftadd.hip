@@ -764,6 +764,7 @@ struct BatchArgs {
     int terms;                 // additive: T
     const int8_t* blk_exps;    // block-wise: [q][NB][K/8]
     int row_block, NB;         // block-wise
+    const int8_t* col_exps;    // column-wise: [q][K]
 };
 
 // One piece for this lane: KW key words of Q planes, their exponents, and the
@@ -775,6 +776,7 @@ struct BatchJob {
     uint4 xr;
     uint32_t et[Q], st[Q];  // additive: T exponent bytes, T term signs
     uint4 eb[Q];            // block-wise: the 16 exponents of the block in the row's block of rows
+    uint2 xe[Q];            // column-wise: the exponents of the table chunk's 8 columns
 };
 
 template <int KW>
@@ -797,13 +799,16 @@ __device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
     asm volatile("" : "+v"(j.e[i]));
 }
 
-// MODE: kRowWise, kAdditive (each plane's group sums shifted by T signed terms)
-// or kBlockWise (each queried entry shifted by its key's exponent).
+// MODE: kRowWise, kAdditive (each plane's group sums shifted by T signed terms),
+// kBlockWise (each queried entry shifted by its key's exponent) or kColWise
+// (each plane queries its own tables, built in turn from the activations
+// shifted by that plane's column exponents; the queried sums need no shift).
 template <int Q, int KW, int MODE>
 __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
     constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
     constexpr bool ADD = MODE == kAdditive;
     constexpr bool BLK = MODE == kBlockWise;
+    constexpr bool COL = MODE == kColWise;
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4;
@@ -859,6 +864,11 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
             for (int i = 0; i < Q; ++i)
                 j.eb[i] = *reinterpret_cast<const uint4*>(a.blk_exps +
                                                           ((int64_t)i * a.NB + rb) * C + 16 * J);
+        } else if constexpr (COL) {
+#pragma unroll
+            for (int i = 0; i < Q; ++i)
+                j.xe[i] = *reinterpret_cast<const uint2*>(a.col_exps + (int64_t)i * a.K +
+                                                          8 * (kBlockChunks * J + bc));
         } else {
             const int8_t* e = exp_row + (bpg == 1 ? J : J / bpg);
 #pragma unroll
@@ -870,13 +880,19 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
         for (int i = 0; i < Q; ++i) load_words<KW>(kp + (int64_t)i * a.N * C, j.w[i]);
     };
-    auto build = [&](const uint4 xr) {
+    auto build = [&](const uint4 xr, const uint2 xe) {
         const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
         float f[8];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
             f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
+        }
+        if constexpr (COL) {
+            const uint32_t e2[2] = {xe.x, xe.y};
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                f[t] = ldexpf(f[t], (int)(int8_t)(e2[t >> 2] >> (8 * (t & 3))));
         }
         float lo[16], hi[16];
         nibble_sums(f[0], f[1], f[2], f[3], lo);
@@ -900,6 +916,9 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
         for (int i = 0; i < Q; ++i) {
             __builtin_amdgcn_sched_barrier(0);
+            // column-wise: this plane's tables replace the previous plane's
+            // (the wave's LDS reads and writes complete in order)
+            if constexpr (COL) build(j.xr, j.xe[i]);
             pin_batch_plane<Q, KW>(j, i);
             float s[kQuad];
             // block-wise: the exponents of this lane's KW key words (4 keys each),
@@ -959,7 +978,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                 // the word's adds complete here, so its loads' registers free up
                 asm volatile("" : "+v"(s[0]), "+v"(s[1]), "+v"(s[2]), "+v"(s[3]));
             }
-            if constexpr (BLK) {
+            if constexpr (BLK || COL) {
 #pragma unroll
                 for (int u = 0; u < kQuad; ++u) tot[u] += s[u] * keep;
             } else if constexpr (ADD) {
@@ -989,11 +1008,11 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     BatchJob<Q, KW> ja, jb;
     load_job(0, ja);
     for (int pc = 0; pc < pieces; pc += 2) {
-        build(ja.xr);
+        if constexpr (!COL) build(ja.xr, uint2{});
         load_job(imin(pc + 1, pieces - 1), jb);
         query_job(pc, ja);
         if (pc + 1 >= pieces) break;
-        build(jb.xr);
+        if constexpr (!COL) build(jb.xr, uint2{});
         load_job(imin(pc + 2, pieces - 1), ja);
         query_job(pc + 1, jb);
     }
@@ -1112,14 +1131,15 @@ int rows_workgroups(int q, int N) {
 // table build about 1144 (eight waves of 32 four-byte writes, which cost about
 // four times as much per byte as the reads); a CU runs ceil(workgroups / 256)
 // workgroups.  The KW with the least LDS work on the busiest CU wins.
-int batch_kw(int q, int N, int batch) {
+int batch_kw(int q, int N, int batch, int builds = 1) {
     const int64_t quads = (batch + kQuad - 1) / kQuad;
     int best_kw = 1;
     double best = -1;
     for (int kw = 1; kw <= 4; kw <<= 1) {
         const int64_t rows = 16 * kw;
         const int64_t wgs = (N + rows - 1) / rows * quads;
-        const double cost = (double)((wgs + 255) / 256) * (16.5 * (double)rows * q + 1144.0);
+        const double cost =
+            (double)((wgs + 255) / 256) * (16.5 * (double)rows * q + 1144.0 * builds);
         if (best < 0 || cost < best) {
             best = cost;
             best_kw = kw;
@@ -1128,11 +1148,11 @@ int batch_kw(int q, int N, int batch) {
     return best_kw;
 }
 
-void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
+void make_plan(int q, int N, int K, int group, int batch, sa_plan* p, int builds = 1) {
     *p = sa_plan{};
     p->threads = kThreads;
     if (group % 128 == 0 && batch >= 2) {
-        const int kw = batch_kw(q, N, batch);
+        const int kw = batch_kw(q, N, batch, builds);
         const int tiles = (N + 16 * kw - 1) / (16 * kw);
         const int quads = (batch + kQuad - 1) / kQuad;
         p->path = 2;
@@ -1161,10 +1181,14 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p) {
     p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
-// Column-wise factors: the row kernel with one plane per job (path 3).
+// Column-wise factors: the row kernel with one plane per job (path 3, batch
+// 1), or the batch kernel building each plane's tables in turn (path 6).
 void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
-    (void)q;
-    (void)batch;
+    if (batch >= 2) {
+        make_plan(q, N, K, 128, batch, p, q);
+        p->path = 6;
+        return;
+    }
     *p = sa_plan{};
     const int groups = (N + kGroupRows - 1) / kGroupRows;
     const int wgs = rows_workgroups(1, N);
@@ -1484,6 +1508,25 @@ SA_API int sa_shiftadd_gemm_colwise(const uint16_t* x, const uint8_t* packed_bit
         return SA_ERR_ALIGN;
     sa_plan plan;
     make_plan_colwise(q, N, K, batch, &plan);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (plan.path == 6) {
+        BatchArgs a{};
+        a.x = x;
+        a.packed = packed_bits;
+        a.exps = col_exps;  // not read in this mode
+        a.col_exps = col_exps;
+        a.q = q;
+        a.N = N;
+        a.K = K;
+        a.G = K;
+        a.B = batch;
+        a.y = y;
+        const int kw = plan.rows_per_wg / 16;
+        a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
+        a.n_quads = (batch + kQuad - 1) / kQuad;
+        launch_batch<kColWise>(q, kw, a, plan.workgroups, s);
+        return launch_status();
+    }
     RowsArgs a{};
     a.x = x;
     a.packed = packed_bits;
@@ -1496,8 +1539,7 @@ SA_API int sa_shiftadd_gemm_colwise(const uint16_t* x, const uint8_t* packed_bit
     a.B = batch;
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
-    hipLaunchKernelGGL(k_gemm_rows_col, dim3(plan.workgroups), dim3(kRowThreads), 0,
-                       reinterpret_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k_gemm_rows_col, dim3(plan.workgroups), dim3(kRowThreads), 0, s, a);
     return launch_status();
 }
 

@@ -196,6 +196,8 @@ def test_colwise_validation_codes():
     p = sa.sa_plan_gemm_colwise(3, 4096, 4096, 1)
     assert p["path"] == 3 and p["workgroups"] == 256 and p["pieces"] == 1
     assert sa.sa_plan_gemm_colwise(3, 8192, 28672, 1)["pieces"] == 7
+    p = sa.sa_plan_gemm_colwise(3, 4096, 4096, 16)  # the batch kernel, one build per plane
+    assert p["path"] == 6 and p["rows_per_wg"] == 64
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm_colwise(3, 100, 200, 1)
 

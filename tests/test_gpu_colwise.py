@@ -136,3 +136,53 @@ def test_colwise_error_codes():
                                     dev(c200["col_exps"]), 2, 64, 200, 1, y)
     with pytest.raises(sa.SaError):
         sa.sa_shiftadd_gemm_colwise(dev(c["x"]), packed, dev(c["col_exps"]), 9, 64, 256, 1, y)
+
+
+# Batch >= 2 runs the batch kernel (plan path 6): each plane's tables are built
+# in turn from the shifted activations; 16, 32 or 64 rows per workgroup.
+BATCH_CASES = [
+    # (q, N, K, B, label)
+    (3, 1000, 1024, 8, "KW=1, two quads"),
+    (3, 4096, 1024, 8, "KW=2"),
+    (4, 4096, 512, 16, "KW=4, four planes"),
+    (8, 2048, 512, 16, "eight planes"),
+    (2, 130, 384, 5, "ragged quad and rows"),
+    (1, 77, 4224, 6, "one plane, ragged last piece"),
+    (5, 300, 2048, 13, "five planes, two pieces, ragged quad"),
+]
+
+
+@pytest.mark.parametrize("q,N,K,B,label", BATCH_CASES, ids=[c[-1] for c in BATCH_CASES])
+def test_colwise_batch_parity(q, N, K, B, label):
+    plan = sa.sa_plan_gemm_colwise(q, N, K, B)
+    assert plan["path"] == 6
+    say(f"colwise batch q={q} N={N} K={K} B={B} rows/wg={plan['rows_per_wg']}: {label}")
+    c = workloads.colwise_case(q, N, K, B, seed=q + N + K + B)
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_colwise(c["x"], c["signs"], c["col_exps"])
+    check(y, y_ref, a_ref, label)
+
+
+def test_colwise_batch_rows_agree_with_batch_one():
+    """Batch rows of the batch kernel against the row kernel on each row alone."""
+    q, N, K, B = 3, 1024, 2048, 8
+    c = workloads.colwise_case(q, N, K, B, seed=5)
+    packed = sa.pack_weights(dev(c["signs"]))
+    y = run(c, packed)
+    y_ref, a_ref = oracle.shiftadd_gemm_colwise(c["x"], c["signs"], c["col_exps"])
+    check(y, y_ref, a_ref, "batch 8")
+    for b in (0, 3, 7):
+        y1 = run(dict(c, B=1, x=c["x"][b:b + 1]), packed)
+        check(y1, y_ref[b:b + 1], a_ref[b:b + 1], f"batch row {b} alone")
+
+
+@pytest.mark.parametrize("N,K", [(4096, 4096), (11008, 4096)])
+def test_colwise_batch_full_size_sampled(N, K):
+    q, B = 3, 16
+    say(f"colwise batch full size N={N} K={K} B={B}")
+    c = workloads.colwise_case(q, N, K, B, seed=2)
+    y = run(c)
+    rows = np.sort(np.random.default_rng(1).choice(N, 256, replace=False))
+    rows[-1] = N - 1
+    y_ref, a_ref = oracle.shiftadd_gemm_colwise(c["x"], c["signs"], c["col_exps"], rows=rows)
+    check(y[:, rows], y_ref, a_ref, f"{N}x{K} batch {B} sampled")
