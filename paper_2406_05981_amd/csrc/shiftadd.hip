@@ -375,6 +375,12 @@ __device__ inline void pin_terms(JobRegs<Q>& j, int i) {
     asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
 }
 
+// Software-pipelined table reads need 8 more registers: used where they stay
+// within the 128 registers of four waves per SIMD (up to 3 planes, one shift
+// per plane); block-wise shifts per key keep the plain order.
+template <int Q, bool BLK>
+constexpr bool kPipelineWords = Q <= 3 && !BLK;
+
 // Queries and adds of one job: sum over planes of ldexp(block sum, exponent).
 // Planes are consumed in load order, so a plane's queries run while later
 // planes are still arriving.
@@ -395,8 +401,22 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
         uint32_t ek[4];
         if constexpr (BLK) rotate16(j.eb[i], r, ek);
         float acc;
-#pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
+        auto add_key = [&](int wd, int t, float L, float H) {
+            if constexpr (BLK) {
+                const float v = ldexpf(L + H, (int)(int8_t)(ek[wd] >> (8 * t)));
+                if (wd == 0 && t == 0)
+                    acc = v;
+                else
+                    acc += v;
+            } else if (wd == 0 && t == 0) {
+                acc = L + H;
+            } else {
+                acc += L;
+                acc += H;
+            }
+        };
+        // the 8 table reads of key word wd (4 keys, low and high half)
+        auto fetch = [&](int wd, float* Lo, float* Ho) {
             // row byte of each of 4 keys: low nibble | region << 4, and
             // high nibble (in place) | region
             const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn_lo;
@@ -405,21 +425,38 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
             for (int t = 0; t < 4; ++t) {
                 // byte 0: slot offset (offs byte t); byte 1: row (byte t)
                 const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
-                const float L = *reinterpret_cast<const float*>(
+                Lo[t] = *reinterpret_cast<const float*>(
                     lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
-                const float H = *reinterpret_cast<const float*>(
+                Ho[t] = *reinterpret_cast<const float*>(
                     lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
-                if constexpr (BLK) {
-                    const float v = ldexpf(L + H, (int)(int8_t)(ek[wd] >> (8 * t)));
-                    if (wd == 0 && t == 0)
-                        acc = v;
-                    else
-                        acc += v;
-                } else if (wd == 0 && t == 0) {
-                    acc = L + H;
-                } else {
-                    acc += L;
-                    acc += H;
+            }
+        };
+        if constexpr (kPipelineWords<Q, BLK>) {
+            // Word wd + 1's reads go out before word wd's adds: a wave keeps
+            // up to 16 table reads in flight instead of draining 8 at a time.
+            float Lw[2][4], Hw[2][4];
+            fetch(0, Lw[0], Hw[0]);
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+                if (wd + 1 < 4) fetch(wd + 1, Lw[(wd + 1) & 1], Hw[(wd + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) add_key(wd, t, Lw[wd & 1][t], Hw[wd & 1][t]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+                const uint32_t lo = (words[wd] & 0x0f0f0f0fu) | rgn_lo;
+                const uint32_t hi = (words[wd] & 0xf0f0f0f0u) | rgn_hi;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                    const float L = *reinterpret_cast<const float*>(
+                        lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
+                    const float H = *reinterpret_cast<const float*>(
+                        lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
+                    add_key(wd, t, L, H);
                 }
             }
         }
