@@ -840,7 +840,10 @@ __device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
 // kBlockWise (each queried entry shifted by its key's exponent) or kColWise
 // (each plane queries its own tables, built in turn from the activations
 // shifted by that plane's column exponents; the queried sums need no shift).
-template <int Q, int KW, int MODE>
+// UNI (block-wise): the workgroup's rows lie in one block of rows, so the
+// block exponents are the same for all its lanes and come in by scalar loads,
+// which keeps them out of the vector registers.
+template <int Q, int KW, int MODE, bool UNI = false>
 __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
     constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
     constexpr bool ADD = MODE == kAdditive;
@@ -895,6 +898,12 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                 j.et[i] = load_terms(a.exps + i * plane + off, a.terms);
                 j.st[i] = load_terms(a.term_signs + i * plane + off, a.terms);
             }
+        } else if constexpr (BLK && UNI) {
+            const int Ju = __builtin_amdgcn_readfirstlane(J);  // J is uniform per wave
+            const int8_t* eb = a.blk_exps + (int64_t)(row0 / a.row_block) * C + 16 * Ju;
+#pragma unroll
+            for (int i = 0; i < Q; ++i)
+                j.eb[i] = *reinterpret_cast<const uint4*>(eb + (int64_t)i * a.NB * C);
         } else if constexpr (BLK) {
             const int rb = n / a.row_block;
 #pragma unroll
@@ -1077,19 +1086,23 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     }
 }
 
-template <int Q, int KW, int MODE = kRowWise>
+// UNI (block-wise only): every workgroup's rows lie in one block of rows
+// (row_block is a multiple of the 16*KW rows of a workgroup).
+template <int Q, int KW, int MODE = kRowWise, bool UNI = false>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_batch(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];  // 64 KB
     __shared__ float4 red[kRowWaves * kBatchRows];            // 8 KB
-    gemm_batch_body<Q, KW, MODE>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE, UNI>(a, reinterpret_cast<float*>(lut),
+                                      reinterpret_cast<float*>(red));
 }
 
-template <int Q, int KW, int MODE = kRowWise>
+template <int Q, int KW, int MODE = kRowWise, bool UNI = false>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_batch_wide(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];
     __shared__ float4 red[kRowWaves * kBatchRows];
-    gemm_batch_body<Q, KW, MODE>(a, reinterpret_cast<float*>(lut), reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE, UNI>(a, reinterpret_cast<float*>(lut),
+                                      reinterpret_cast<float*>(red));
 }
 
 // ---------------------------------------------------------------- read probe
@@ -1168,11 +1181,11 @@ int rows_workgroups(int q, int N) {
 // table build about 1144 (eight waves of 32 four-byte writes, which cost about
 // four times as much per byte as the reads); a CU runs ceil(workgroups / 256)
 // workgroups.  The KW with the least LDS work on the busiest CU wins.
-int batch_kw(int q, int N, int batch, int builds = 1) {
+int batch_kw(int q, int N, int batch, int builds = 1, int max_kw = 4) {
     const int64_t quads = (batch + kQuad - 1) / kQuad;
     int best_kw = 1;
     double best = -1;
-    for (int kw = 1; kw <= 4; kw <<= 1) {
+    for (int kw = 1; kw <= max_kw; kw <<= 1) {
         const int64_t rows = 16 * kw;
         const int64_t wgs = (N + rows - 1) / rows * quads;
         const double cost =
@@ -1185,11 +1198,12 @@ int batch_kw(int q, int N, int batch, int builds = 1) {
     return best_kw;
 }
 
-void make_plan(int q, int N, int K, int group, int batch, sa_plan* p, int builds = 1) {
+void make_plan(int q, int N, int K, int group, int batch, sa_plan* p, int builds = 1,
+               int max_kw = 4) {
     *p = sa_plan{};
     p->threads = kThreads;
     if (group % 128 == 0 && batch >= 2) {
-        const int kw = batch_kw(q, N, batch, builds);
+        const int kw = batch_kw(q, N, batch, builds, max_kw);
         const int tiles = (N + 16 * kw - 1) / (16 * kw);
         const int quads = (batch + kQuad - 1) / kQuad;
         p->path = 2;
@@ -1238,9 +1252,14 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
 }
 
 // Block-wise factors: the row kernel (batch 1, path 4) or the batch kernel
-// (batch >= 2, path 5) with a shift per key.
-void make_plan_blockwise(int q, int N, int K, int batch, sa_plan* p) {
-    make_plan(q, N, K, 128, batch, p);
+// (batch >= 2, path 5) with a shift per key.  The batch kernel holds each
+// job's 16 key exponents per plane in scalar registers when row_block is a
+// multiple of its 16*KW rows, else in vector registers.  With 4 planes KW is
+// capped at 2: at 4 key words per lane the variant does not fit the vector
+// registers of four waves per SIMD (measured slower than 2 key words).
+void make_plan_blockwise(int q, int N, int K, int row_block, int batch, sa_plan* p) {
+    (void)row_block;
+    make_plan(q, N, K, 128, batch, p, 1, q == 4 ? 2 : 4);
     p->path = batch >= 2 ? 5 : 4;
 }
 
@@ -1267,26 +1286,26 @@ void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
     }
 }
 
-template <int KW, int MODE>
+template <int KW, int MODE, bool UNI>
 void launch_batch_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
     const dim3 g(workgroups), b(kRowThreads);
     switch (q) {
-        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE>), g, b, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE>), g, b, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE>), g, b, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW, MODE>), g, b, 0, s, a); break;
-        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW, MODE>), g, b, 0, s, a); break;
-        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW, MODE>), g, b, 0, s, a); break;
-        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW, MODE>), g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW, MODE>), g, b, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW, MODE, UNI>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW, MODE, UNI>), g, b, 0, s, a); break;
     }
 }
 
-template <int MODE = kRowWise>
+template <int MODE = kRowWise, bool UNI = false>
 void launch_batch(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t s) {
-    if (kw == 4) launch_batch_kw<4, MODE>(q, a, workgroups, s);
-    else if (kw == 2) launch_batch_kw<2, MODE>(q, a, workgroups, s);
-    else launch_batch_kw<1, MODE>(q, a, workgroups, s);
+    if (kw == 4) launch_batch_kw<4, MODE, UNI>(q, a, workgroups, s);
+    else if (kw == 2) launch_batch_kw<2, MODE, UNI>(q, a, workgroups, s);
+    else launch_batch_kw<1, MODE, UNI>(q, a, workgroups, s);
 }
 
 }  // namespace
@@ -1399,7 +1418,7 @@ SA_API int sa_plan_gemm_blockwise(int q, int N, int K, int row_block, int batch,
     const int st = check_dims(q, N, K);
     if (st != SA_OK) return st;
     if (batch < 1 || batch > SA_MAX_BATCH || (K % 128) || row_block < 1) return SA_ERR_SHAPE;
-    make_plan_blockwise(q, N, K, batch, plan);
+    make_plan_blockwise(q, N, K, row_block, batch, plan);
     return SA_OK;
 }
 
@@ -1413,7 +1432,7 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
     if (!aligned16(x) || !aligned16(packed_bits) || !aligned16(y) || !aligned16(blk_exps))
         return SA_ERR_ALIGN;
     sa_plan plan;
-    make_plan_blockwise(q, N, K, batch, &plan);
+    make_plan_blockwise(q, N, K, row_block, batch, &plan);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (plan.path == 5) {
         BatchArgs a{};
@@ -1432,7 +1451,10 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
         const int kw = plan.rows_per_wg / 16;
         a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
         a.n_quads = (batch + kQuad - 1) / kQuad;
-        launch_batch<kBlockWise>(q, kw, a, plan.workgroups, s);
+        if (row_block % plan.rows_per_wg == 0)
+            launch_batch<kBlockWise, true>(q, kw, a, plan.workgroups, s);
+        else
+            launch_batch<kBlockWise, false>(q, kw, a, plan.workgroups, s);
         return launch_status();
     }
     RowsArgs a{};

@@ -135,12 +135,18 @@ def test_blockwise_error_codes():
 
 # Batch >= 2 runs the batch kernel (plan path 5): 16, 32 or 64 rows per
 # workgroup (KW = 1, 2, 4 key words per lane) and four batch rows per table.
+# When row_block is a multiple of the workgroup's rows the block exponents
+# come in by scalar loads ("uniform"), else per lane.
 BATCH_CASES = [
     # (q, N, K, B, row_block, label)
-    (3, 1000, 1024, 8, 125, "KW=1, two quads"),
-    (3, 4096, 1024, 8, 512, "KW=2"),
-    (4, 4096, 512, 16, 512, "KW=4, four planes"),
-    (8, 2048, 512, 16, 256, "KW=2, eight planes"),
+    (3, 1000, 1024, 8, 125, "KW=1, two quads, per lane"),
+    (3, 4096, 1024, 8, 512, "KW=2, uniform"),
+    (4, 4096, 512, 16, 512, "four planes (KW capped at 2), uniform"),
+    (3, 4096, 2048, 16, 512, "KW=4, uniform"),
+    (2, 4096, 1024, 16, 100, "KW=4, per lane"),
+    (3, 4000, 1024, 16, 512, "uniform, ragged last tile"),
+    (3, 4000, 1024, 16, 1000, "KW=4, q=3, per lane"),
+    (8, 2048, 512, 16, 256, "KW=2, eight planes, uniform"),
     (2, 130, 384, 5, 17, "ragged quad and rows, 17-row blocks"),
     (1, 77, 4224, 6, 1, "a factor per row, ragged last piece"),
     (5, 300, 2048, 13, 40, "five planes, two pieces, ragged quad"),
@@ -151,6 +157,7 @@ BATCH_CASES = [
 def test_blockwise_batch_parity(q, N, K, B, rb, label):
     plan = sa.sa_plan_gemm_blockwise(q, N, K, rb, B)
     assert plan["path"] == 5
+    assert ("uniform" in label) == (rb % plan["rows_per_wg"] == 0)
     say(f"blockwise batch q={q} N={N} K={K} B={B} row_block={rb} "
         f"rows/wg={plan['rows_per_wg']}: {label}")
     c = workloads.blockwise_case(q, N, K, B, rb, seed=q + N + K + B + rb)
