@@ -482,7 +482,7 @@ def bench_criterion(args) -> int:
 
     us_gram = timed(gram, steps)
     us_all = timed(chain, steps)
-    tiles = (K // 64) * (K // 64 + 1) // 2
+    tiles = (K // 128) * (K // 128 + 1) // 2  # 128 x 128 lower-triangular tiles
     flops_alg = K * (K + 1) * T          # the unique entries of X X^T, 2 flops per product
     tflops = flops_alg / us_gram / 1e6
     log(f"gram {us_gram:.1f} us ({tflops:.1f} TFLOP/s), whole criterion {us_all:.1f} us; "

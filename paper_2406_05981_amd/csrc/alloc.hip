@@ -31,10 +31,12 @@ namespace {
 
 constexpr int kGT = 128;       // output tile: 128 x 128
 constexpr int kGK = 32;        // calibration columns per stage
-constexpr int kGPad = kGK + 4; // LDS row stride in halves (72 bytes): spreads rows over banks
+// LDS row stride in halves (80 bytes): 16-byte aligned rows whose 16-byte
+// operand reads by 16 consecutive rows cover all 64 banks once
+constexpr int kGPad = kGK + 8;
 constexpr int kGBuf = kGT * kGPad;
 
-typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 // Tile (ti, tj), ti >= tj, of H = X X^T for X fp16 [K][T] row-major.  Four
@@ -42,9 +44,11 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 // four floats).  The two 128 x 32 slices of X of a stage are double-buffered
 // in LDS; the next stage's slices are loaded into registers while the current
 // one is multiplied, so one barrier per stage suffices.
-// Operand layout of v_mfma_f32_16x16x16_f16: lane l holds row (l mod 16) of A
-// and column (l mod 16) of B at k = 4 (l / 16) .. 4 (l / 16) + 3; the result
-// holds rows 4 (l / 16) .. + 3 of column (l mod 16).
+// Operand layout of v_mfma_f32_16x16x32_f16 (gfx950; twice the products per
+// instruction of the 16x16x16 form at about the same issue cost, measured):
+// lane l holds row (l mod 16) of A and column (l mod 16) of B at
+// k = 8 (l / 16) .. 8 (l / 16) + 7; the result holds rows 4 (l / 16) .. + 3 of
+// column (l mod 16).
 __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x, int K, int T,
                                                   float* __restrict__ H) {
     __shared__ uint16_t sa[2 * kGBuf];
@@ -68,7 +72,7 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
     for (int u = 0; u < 4; ++u)
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc[u][v] = float4v{0.f, 0.f, 0.f, 0.f};
-    const int r16 = lane & 15, kq = (lane >> 4) * 4;
+    const int r16 = lane & 15, kq = (lane >> 4) * 8;
 
     uint4 ra0 = *reinterpret_cast<const uint4*>(pa);
     uint4 ra1 = *reinterpret_cast<const uint4*>(pa + half);
@@ -77,14 +81,10 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
     auto stage_store = [&](int buf) {
         uint16_t* A = sa + buf * kGBuf;
         uint16_t* Bm = sb + buf * kGBuf;
-        *reinterpret_cast<uint2*>(A + lr * kGPad + lc) = make_uint2(ra0.x, ra0.y);
-        *reinterpret_cast<uint2*>(A + lr * kGPad + lc + 4) = make_uint2(ra0.z, ra0.w);
-        *reinterpret_cast<uint2*>(A + (lr + 64) * kGPad + lc) = make_uint2(ra1.x, ra1.y);
-        *reinterpret_cast<uint2*>(A + (lr + 64) * kGPad + lc + 4) = make_uint2(ra1.z, ra1.w);
-        *reinterpret_cast<uint2*>(Bm + lr * kGPad + lc) = make_uint2(rb0.x, rb0.y);
-        *reinterpret_cast<uint2*>(Bm + lr * kGPad + lc + 4) = make_uint2(rb0.z, rb0.w);
-        *reinterpret_cast<uint2*>(Bm + (lr + 64) * kGPad + lc) = make_uint2(rb1.x, rb1.y);
-        *reinterpret_cast<uint2*>(Bm + (lr + 64) * kGPad + lc + 4) = make_uint2(rb1.z, rb1.w);
+        *reinterpret_cast<uint4*>(A + lr * kGPad + lc) = ra0;
+        *reinterpret_cast<uint4*>(A + (lr + 64) * kGPad + lc) = ra1;
+        *reinterpret_cast<uint4*>(Bm + lr * kGPad + lc) = rb0;
+        *reinterpret_cast<uint4*>(Bm + (lr + 64) * kGPad + lc) = rb1;
     };
     stage_store(0);
     __syncthreads();
@@ -101,20 +101,20 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
         const uint16_t* A = sa + buf * kGBuf;
         const uint16_t* Bm = sb + buf * kGBuf;
 #pragma unroll
-        for (int ks = 0; ks < kGK; ks += 16) {
-            half4 av[4], bv[4];
+        for (int ks = 0; ks < kGK; ks += 32) {
+            half8 av[4], bv[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                av[u] = __builtin_bit_cast(half4, *reinterpret_cast<const uint2*>(
+                av[u] = __builtin_bit_cast(half8, *reinterpret_cast<const uint4*>(
                                                       A + (wi + 16 * u + r16) * kGPad + ks + kq));
-                bv[u] = __builtin_bit_cast(half4, *reinterpret_cast<const uint2*>(
+                bv[u] = __builtin_bit_cast(half8, *reinterpret_cast<const uint4*>(
                                                       Bm + (wj + 16 * u + r16) * kGPad + ks + kq));
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x16f16(av[u], bv[v], acc[u][v], 0, 0, 0);
+                    acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[u], bv[v], acc[u][v], 0, 0, 0);
         }
         if (st + 1 < stages) stage_store(buf ^ 1);
         __syncthreads();
