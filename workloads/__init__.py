@@ -130,6 +130,13 @@ WORKLOADS: Dict[str, Workload] = {
             "down 4096x11008) with per-layer q in {2,3,4}, mean 3 over layers, G=128, "
             "exps in [-10,-3], x ~ N(0,1) with 1% of channels x20, replicated over 32 layers",
             _layer_set(0), 128, (-10, -3), 0.01, 20.0, (1, 4, 8, 16), depth=32),
+        Workload(
+            "llama2_70b_mlp_shard8", 5,
+            "One GPU's shard of the LLaMA-2-70B-shaped MLP split 8 ways: up 3584x8192 "
+            "(rows split) and down 8192x3584 (columns split), q=3, G=128, exps in [-12,-3], "
+            "x ~ N(0,1)",
+            (Layer("up_shard", 3584, 8192, 3), Layer("down_shard", 8192, 3584, 3)),
+            128, (-12, -3), 0.0, 1.0, (1, 8)),
     )
 }
 
