@@ -485,21 +485,27 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
 // that plane's column exponents (exact in fp32), and the queried sums need no
 // shift.  MODE kBlockWise: one exponent per (plane, block of rows, key); each
 // queried entry is shifted (job_sum).
-template <int Q, int U, int MODE>
+// H = 2 (layers of several pieces with at most one workgroup per CU): 16
+// waves, the second 8 taking the odd pieces with their own 64 KB of tables, so
+// two pieces are in flight per CU; the 16 waves' row sums meet at the end.
+template <int Q, int U, int MODE, int H = 1>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     constexpr bool COL = MODE == kColWise;
     constexpr bool BLK = MODE == kBlockWise;
     constexpr bool ADD = MODE == kAdditive;
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave_all = threadIdx.x >> 6;
+    const int half = H == 1 ? 0 : wave_all / kRowWaves;  // pieces half, half + H, ...
+    const int wave = wave_all - half * kRowWaves;
     const int r = lane & 15, p = lane >> 4, part = 4 * wave + p;
     // row groups of this workgroup: the first `extra` workgroups take one more
     const int wgs = (int)gridDim.x, wg = (int)blockIdx.x;
     const int base = a.groups / wgs, extra = a.groups - base * wgs;
     const int nrg = base + (wg < extra ? 1 : 0);
     const int rg0 = wg * base + imin(wg, extra);
-    const int pieces = (C16 + kPieceBlocks - 1) / kPieceBlocks;
+    const int pieces_all = (C16 + kPieceBlocks - 1) / kPieceBlocks;
+    const int pieces = (pieces_all - half + H - 1) / H;  // this half's pieces
     const int planes = COL ? a.q : 1;
     const int jobs = a.B * planes * pieces * nrg;
 
@@ -522,9 +528,13 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 #pragma unroll
     for (int g = 0; g < kMaxRG; ++g) acc[g] = 0.0f;
 
+    lut += half * (16 * kRegionFloats);
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
+    // j.pc counts this half's pieces; the piece itself is H * j.pc + half
     auto row_of = [&](const JobPos& j) { return imin(kGroupRows * (rg0 + j.g) + r, a.N - 1); };
-    auto block_of = [&](const JobPos& j) { return imin(kPieceBlocks * j.pc + part, C16 - 1); };
+    auto block_of = [&](const JobPos& j) {
+        return imin(kPieceBlocks * (H * j.pc + half) + part, C16 - 1);
+    };
     // Tables are wave-local: the 64 lanes of a wave build the 64 chunks of the
     // four blocks that wave queries (lane (r, p) builds chunk r of block
     // `part`), so no table write is ever read by another wave and the only
@@ -535,7 +545,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // activations of this lane's table chunk (and, column-wise, their
     // exponents in the job's plane)
     auto chunk_of = [&](const JobPos& j) {
-        return imin(kPieceChunks * j.pc + kBlockChunks * part + r, C - 1);
+        return imin(kPieceChunks * (H * j.pc + half) + kBlockChunks * part + r, C - 1);
     };
     auto load_x = [&](const JobPos& j) {
         return *reinterpret_cast<const uint4*>(a.x + (int64_t)j.b * a.K + 8 * chunk_of(j));
@@ -603,7 +613,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // queries of one job, accumulation into its row group, and -- when the job
     // completes batch row b -- the combination of the 32 lanes of every row
     auto run_job = [&](const JobPos& j, JobRegs<Q>& regs) {
-        const bool valid = kPieceBlocks * j.pc + part < C16;
+        const bool valid = kPieceBlocks * (H * j.pc + half) + part < C16;
         const float v = job_sum<Q, BLK>(regs, rgn_lo, rgn_hi, offs, lut_bytes, r,
                                         ADD ? a.terms : 0);
 #pragma unroll
@@ -616,17 +626,17 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                     float s = acc[gg];
                     s += __shfl_xor(s, 16);
                     s += __shfl_xor(s, 32);
-                    if (lane < kGroupRows) red[wave][kGroupRows * gg + r] = s;
+                    if (lane < kGroupRows) red[wave_all][kGroupRows * gg + r] = s;
                 }
                 acc[gg] = 0.0f;
             }
             __syncthreads();
-            for (int t = threadIdx.x; t < kGroupRows * nrg; t += kRowThreads) {
+            for (int t = threadIdx.x; t < kGroupRows * nrg; t += kRowThreads * H) {
                 const int n = kGroupRows * rg0 + t;
                 if (n < a.N) {
                     float s = red[0][t];
 #pragma unroll
-                    for (int w = 1; w < kRowWaves; ++w) s += red[w][t];
+                    for (int w = 1; w < kRowWaves * H; ++w) s += red[w][t];
                     a.y[(int64_t)j.b * a.N + n] = s;
                 }
             }
@@ -694,12 +704,12 @@ constexpr int rows_jobs_per_iter() { return 1; }
 
 // Up to 4 planes: two 8-wave workgroups per CU (4 waves per SIMD, <= 128
 // VGPRs).  More planes need more registers: one workgroup per CU.
-template <int Q>
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+template <int Q, int H = 1>
+__global__ __launch_bounds__(kRowThreads * H) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_rows(RowsArgs a) {
-    __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise>(a, lut, red);
+    __shared__ float lut[H * 16 * kRegionFloats];  // 64 KB per half
+    __shared__ float red[kRowWaves * H][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise, H>(a, lut, red);
 }
 
 template <int Q>
@@ -710,20 +720,21 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
 }
 
 // Column-wise factors: one plane per job, registers of a one-plane job.
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+template <int H = 1>
+__global__ __launch_bounds__(kRowThreads * H) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_rows_col(RowsArgs a) {
-    __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<1, 1, kColWise>(a, lut, red);
+    __shared__ float lut[H * 16 * kRegionFloats];  // 64 KB per half
+    __shared__ float red[kRowWaves * H][kGroupRows * kMaxRG];
+    gemm_rows_body<1, 1, kColWise, H>(a, lut, red);
 }
 
 // Block-wise factors: the row kernel with a shift per queried key.
-template <int Q>
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+template <int Q, int H = 1>
+__global__ __launch_bounds__(kRowThreads * H) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_rows_blk(RowsArgs a) {
-    __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, 1, kBlockWise>(a, lut, red);
+    __shared__ float lut[H * 16 * kRegionFloats];  // 64 KB per half
+    __shared__ float red[kRowWaves * H][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kBlockWise, H>(a, lut, red);
 }
 
 template <int Q>
@@ -734,12 +745,12 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_blk_wide(RowsArgs a) 
 }
 
 // Additive factors: the row kernel with T signed shifts per plane sum.
-template <int Q>
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
+template <int Q, int H = 1>
+__global__ __launch_bounds__(kRowThreads * H) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_rows_add(RowsArgs a) {
-    __shared__ float lut[16 * kRegionFloats];  // 64 KB
-    __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, 1, kAdditive>(a, lut, red);
+    __shared__ float lut[H * 16 * kRegionFloats];  // 64 KB per half
+    __shared__ float red[kRowWaves * H][kGroupRows * kMaxRG];
+    gemm_rows_body<Q, 1, kAdditive, H>(a, lut, red);
 }
 
 template <int Q>
@@ -1228,8 +1239,12 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p, int builds
     p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);  // the largest share
     p->workgroups = wgs;
     p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
-    p->threads = kRowThreads;
-    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
+    // Two pieces in flight per workgroup (16 waves, 128 KB of tables) where
+    // the workgroups leave a CU to each: up to 4 planes (128 registers at four
+    // waves per SIMD), at most 256 workgroups, several pieces.
+    const int split = (q <= kRowsResidentQ && wgs <= 256 && p->pieces >= 2) ? 2 : 1;
+    p->threads = kRowThreads * split;
+    p->lds_bytes = sizeof(float) * split * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
 // Column-wise factors: the row kernel with one plane per job (path 3, batch
@@ -1247,8 +1262,9 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
     p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);
     p->workgroups = wgs;
     p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
-    p->threads = kRowThreads;
-    p->lds_bytes = sizeof(float) * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
+    const int split = (wgs <= 256 && p->pieces >= 2) ? 2 : 1;  // as in make_plan
+    p->threads = kRowThreads * split;
+    p->lds_bytes = sizeof(float) * split * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);
 }
 
 // Block-wise factors: the row kernel (batch 1, path 4) or the batch kernel
@@ -1260,6 +1276,11 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
 void make_plan_blockwise(int q, int N, int K, int row_block, int batch, sa_plan* p) {
     (void)row_block;
     make_plan(q, N, K, 128, batch, p, 1, q == 4 ? 2 : 4);
+    if (batch < 2 && q == 4 && p->threads == 2 * kRowThreads) {
+        // the 16-wave row kernel with 4 planes and a shift per key spills
+        p->threads = kRowThreads;
+        p->lds_bytes /= 2;
+    }
     p->path = batch >= 2 ? 5 : 4;
 }
 
@@ -1272,8 +1293,17 @@ int grid_for(int64_t items) {
     return (int)g;
 }
 
-void launch_rows(int q, const RowsArgs& a, int workgroups, hipStream_t s) {
-    const dim3 g(workgroups), b(kRowThreads);
+void launch_rows(int q, const RowsArgs& a, int workgroups, int split, hipStream_t s) {
+    const dim3 g(workgroups), b(kRowThreads * split);
+    if (split == 2) {
+        switch (q) {
+            case 1: hipLaunchKernelGGL((k_gemm_rows<1, 2>), g, b, 0, s, a); break;
+            case 2: hipLaunchKernelGGL((k_gemm_rows<2, 2>), g, b, 0, s, a); break;
+            case 3: hipLaunchKernelGGL((k_gemm_rows<3, 2>), g, b, 0, s, a); break;
+            default: hipLaunchKernelGGL((k_gemm_rows<4, 2>), g, b, 0, s, a); break;
+        }
+        return;
+    }
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows<2>, g, b, 0, s, a); break;
@@ -1408,7 +1438,7 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.B = batch;
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
-    launch_rows(q, a, plan.workgroups, s);
+    launch_rows(q, a, plan.workgroups, plan.threads / kRowThreads, s);
     return launch_status();
 }
 
@@ -1470,7 +1500,16 @@ SA_API int sa_shiftadd_gemm_blockwise(const uint16_t* x, const uint8_t* packed_b
     a.groups = (N + kGroupRows - 1) / kGroupRows;
     a.row_block = row_block;
     a.NB = (N + row_block - 1) / row_block;
-    const dim3 g(plan.workgroups), b(kRowThreads);
+    const dim3 g(plan.workgroups), b(plan.threads);
+    if (plan.threads == 2 * kRowThreads) {
+        switch (q) {
+            case 1: hipLaunchKernelGGL((k_gemm_rows_blk<1, 2>), g, b, 0, s, a); break;
+            case 2: hipLaunchKernelGGL((k_gemm_rows_blk<2, 2>), g, b, 0, s, a); break;
+            case 3: hipLaunchKernelGGL((k_gemm_rows_blk<3, 2>), g, b, 0, s, a); break;
+            default: hipLaunchKernelGGL((k_gemm_rows_blk<4, 2>), g, b, 0, s, a); break;
+        }
+        return launch_status();
+    }
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows_blk<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows_blk<2>, g, b, 0, s, a); break;
@@ -1532,7 +1571,16 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
     a.B = batch;
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
-    const dim3 g(plan.workgroups), b(kRowThreads);
+    const dim3 g(plan.workgroups), b(plan.threads);
+    if (plan.threads == 2 * kRowThreads) {
+        switch (q) {
+            case 1: hipLaunchKernelGGL((k_gemm_rows_add<1, 2>), g, b, 0, s, a); break;
+            case 2: hipLaunchKernelGGL((k_gemm_rows_add<2, 2>), g, b, 0, s, a); break;
+            case 3: hipLaunchKernelGGL((k_gemm_rows_add<3, 2>), g, b, 0, s, a); break;
+            default: hipLaunchKernelGGL((k_gemm_rows_add<4, 2>), g, b, 0, s, a); break;
+        }
+        return launch_status();
+    }
     switch (q) {
         case 1: hipLaunchKernelGGL(k_gemm_rows_add<1>, g, b, 0, s, a); break;
         case 2: hipLaunchKernelGGL(k_gemm_rows_add<2>, g, b, 0, s, a); break;
@@ -1598,7 +1646,10 @@ SA_API int sa_shiftadd_gemm_colwise(const uint16_t* x, const uint8_t* packed_bit
     a.B = batch;
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
-    hipLaunchKernelGGL(k_gemm_rows_col, dim3(plan.workgroups), dim3(kRowThreads), 0, s, a);
+    if (plan.threads == 2 * kRowThreads)
+        hipLaunchKernelGGL(k_gemm_rows_col<2>, dim3(plan.workgroups), dim3(plan.threads), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_gemm_rows_col<1>, dim3(plan.workgroups), dim3(plan.threads), 0, s, a);
     return launch_status();
 }
 

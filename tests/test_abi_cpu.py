@@ -198,6 +198,15 @@ def test_colwise_validation_codes():
     assert sa.sa_plan_gemm_colwise(3, 8192, 28672, 1)["pieces"] == 7
     p = sa.sa_plan_gemm_colwise(3, 4096, 4096, 16)  # the batch kernel, one build per plane
     assert p["path"] == 6 and p["rows_per_wg"] == 64
+    # several pieces and at most one workgroup per CU: 16 waves, two pieces at once
+    assert sa.sa_plan_gemm(3, 4096, 11008, 128, 1)["threads"] == 1024
+    assert sa.sa_plan_gemm(4, 3584, 8192, 128, 1)["threads"] == 1024
+    assert sa.sa_plan_gemm(5, 4096, 11008, 128, 1)["threads"] == 512   # registers
+    assert sa.sa_plan_gemm(3, 8192, 28672, 128, 1)["threads"] == 512   # 512 workgroups
+    assert sa.sa_plan_gemm(3, 4096, 4096, 128, 1)["threads"] == 512    # one piece
+    assert sa.sa_plan_gemm_colwise(3, 4096, 11008, 1)["threads"] == 1024
+    assert sa.sa_plan_gemm_blockwise(3, 4096, 11008, 512, 1)["threads"] == 1024
+    assert sa.sa_plan_gemm_blockwise(4, 4096, 11008, 512, 1)["threads"] == 512
     with pytest.raises(sa.SaError):
         sa.sa_plan_gemm_colwise(3, 100, 200, 1)
 

@@ -61,6 +61,9 @@ CASES = [
     (8, 17, 256, 1, 17, "eight planes, one block of rows"),
     (3, 300, 4224, 4, 40, "ragged last piece (33 blocks), batch 4"),
     (5, 200, 1024, 2, 25, "five planes"),
+    (3, 1000, 8320, 1, 125, "16 waves, three pieces, one-block last piece"),
+    (2, 4096, 8192, 1, 512, "16 waves, 256 workgroups"),
+    (4, 1000, 8320, 1, 125, "four planes: 8 waves"),
 ]
 
 

@@ -63,6 +63,8 @@ CASES = [
     (8, 17, 256, 1, "eight planes"),
     (3, 300, 4224, 4, "ragged last piece (33 blocks)"),
     (2, 1000, 2048, 16, "batch 16"),
+    (3, 1000, 8320, 1, "16 waves, three pieces, one-block last piece"),
+    (2, 4096, 8192, 1, "16 waves, 256 workgroups"),
 ]
 
 
