@@ -813,6 +813,7 @@ struct BatchArgs {
     const int8_t* blk_exps;    // block-wise: [q][NB][K/8]
     int row_block, NB;         // block-wise
     const int8_t* col_exps;    // column-wise: [q][K]
+    int pre_bytes;             // PRE: bytes of a lane's exponents over all its pieces
 };
 
 // One piece for this lane: KW key words of Q planes, their exponents, and the
@@ -854,7 +855,14 @@ __device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
 // UNI (block-wise): the workgroup's rows lie in one block of rows, so the
 // block exponents are the same for all its lanes and come in by scalar loads,
 // which keeps them out of the vector registers.
-template <int Q, int KW, int MODE, bool UNI = false>
+// Every wave owns consecutive blocks (J = pieces * wave + pc).  PRE
+// (additive, G = 128, K % 1024 == 0): a lane's T exponent bytes and T term
+// signs of all its pieces are then pieces * T consecutive bytes of its row,
+// fetched by one 4-, 8- or 16-byte load each at the start instead of two
+// scattered loads per piece and plane (these touch one cache line per lane
+// and were a third of the additive kernel's time on large layers; the
+// row-wise kernel's one byte per piece measured no gain from it).
+template <int Q, int KW, int MODE, bool UNI = false, bool PRE = false>
 __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
     constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
     constexpr bool ADD = MODE == kAdditive;
@@ -899,9 +907,43 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     const uint8_t* key_row = a.packed + (int64_t)kTileRows * T * C + 16 * (n & 63) + 4 * KW * dsl;
     const int8_t* exp_row = a.exps + (int64_t)n * NG;
 
+    // PRE: bytes [pieces * wave * T, (pieces * wave + pieces) * T) of the row
+    constexpr int QP = PRE ? Q : 1, QS = (PRE && ADD) ? Q : 1;
+    uint32_t pe[QP][4] = {}, ps[QS][4] = {};
+    if constexpr (PRE) {
+        const int tb = ADD ? a.terms : 1;
+        const int64_t off0 = ((int64_t)n * NG + (int64_t)pieces * wave) * tb;
+        const int64_t plane = (int64_t)a.N * NG * tb;
+        auto fetch = [&](const int8_t* src, uint32_t* w) {
+            if (a.pre_bytes == 16) {
+                const uint4 v = *reinterpret_cast<const uint4*>(src);
+                w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+            } else if (a.pre_bytes == 8) {
+                const uint2 v = *reinterpret_cast<const uint2*>(src);
+                w[0] = v.x; w[1] = v.y;
+            } else {
+                w[0] = *reinterpret_cast<const uint32_t*>(src);
+            }
+        };
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            fetch(a.exps + i * plane + off0, pe[i]);
+            if constexpr (ADD) fetch(a.term_signs + i * plane + off0, ps[QS > 1 ? i : 0]);
+        }
+    }
+    // PRE: the T bytes of piece pc in a lane's preloaded words (T divides 4)
+    auto pre_field = [&](const uint32_t* w, int pc) {
+        const int bo = pc * (ADD ? a.terms : 1);
+        const int wi = bo >> 2;
+        const uint32_t v = wi == 0 ? w[0] : wi == 1 ? w[1] : wi == 2 ? w[2] : w[3];
+        return v >> (8 * (bo & 3));
+    };
+
     auto load_job = [&](int pc, BatchJob<Q, KW>& j) {
-        const int J = imin(kRowWaves * pc + wave, C16 - 1);
-        if constexpr (ADD) {
+        const int J = imin(pieces * wave + pc, C16 - 1);
+        if constexpr (PRE) {
+            // exponents come from the preloaded words at query time
+        } else if constexpr (ADD) {
             const int64_t off = ((int64_t)n * NG + (bpg == 1 ? J : J / bpg)) * a.terms;
             const int64_t plane = (int64_t)a.N * NG * a.terms;
 #pragma unroll
@@ -969,7 +1011,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     float tot[kQuad] = {0.0f, 0.0f, 0.0f, 0.0f};
     auto query_job = [&](int pc, BatchJob<Q, KW>& j) {
         // blocks past the end (last piece) repeat the last block: weight 0
-        const float keep = kRowWaves * pc + wave < C16 ? 1.0f : 0.0f;
+        const float keep = pieces * wave + pc < C16 ? 1.0f : 0.0f;
 #pragma unroll
         for (int i = 0; i < Q; ++i) {
             __builtin_amdgcn_sched_barrier(0);
@@ -1039,6 +1081,10 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
                 for (int u = 0; u < kQuad; ++u) tot[u] += s[u] * keep;
             } else if constexpr (ADD) {
+                if constexpr (PRE) {
+                    j.et[i] = pre_field(pe[i], pc);
+                    j.st[i] = pre_field(ps[QS > 1 ? i : 0], pc);
+                }
                 asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
 #pragma unroll
                 for (int tt = 0; tt < kMaxTerms; ++tt) {
@@ -1053,8 +1099,9 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                     }
                 }
             } else {
+                const int e = PRE ? (int)(int8_t)pre_field(pe[i], pc) : j.e[i];
 #pragma unroll
-                for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
+                for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], e) * keep;
             }
         }
     };
@@ -1099,13 +1146,13 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 
 // UNI (block-wise only): every workgroup's rows lie in one block of rows
 // (row_block is a multiple of the 16*KW rows of a workgroup).
-template <int Q, int KW, int MODE = kRowWise, bool UNI = false>
+template <int Q, int KW, int MODE = kRowWise, bool UNI = false, bool PRE = false>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_batch(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];  // 64 KB
     __shared__ float4 red[kRowWaves * kBatchRows];            // 8 KB
-    gemm_batch_body<Q, KW, MODE, UNI>(a, reinterpret_cast<float*>(lut),
-                                      reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE, UNI, PRE>(a, reinterpret_cast<float*>(lut),
+                                           reinterpret_cast<float*>(red));
 }
 
 template <int Q, int KW, int MODE = kRowWise, bool UNI = false>
@@ -1338,6 +1385,38 @@ void launch_batch(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t
     else launch_batch_kw<1, MODE, UNI>(q, a, workgroups, s);
 }
 
+// Preloaded exponents and term signs (additive batch kernel, up to 3 planes
+// within 128 registers): the bytes a lane needs over all its pieces, or 0
+// where the per-piece loads are used.  Needs G = 128 and K % 1024 == 0 (every
+// wave owns whole blocks, so a lane's bytes stay inside its row), a load of
+// 4, 8 or 16 bytes, and base pointers aligned to it.
+int pre_bytes(int q, int K, int G, int T, const void* p0, const void* p1) {
+    if (G != 128 || K % 1024 || q > 3) return 0;
+    const int pieces = K / 1024;
+    const int lw = pieces * T;
+    if (lw != 4 && lw != 8 && lw != 16) return 0;
+    if ((reinterpret_cast<uintptr_t>(p0) % lw) || (p1 && reinterpret_cast<uintptr_t>(p1) % lw))
+        return 0;
+    return lw;
+}
+
+template <int KW, int MODE>
+void launch_batch_pre_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
+    const dim3 g(workgroups), b(kRowThreads);
+    switch (q) {
+        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, false, true>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, false, true>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, false, true>), g, b, 0, s, a); break;
+    }
+}
+
+template <int MODE>
+void launch_batch_pre(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t s) {
+    if (kw == 4) launch_batch_pre_kw<4, MODE>(q, a, workgroups, s);
+    else if (kw == 2) launch_batch_pre_kw<2, MODE>(q, a, workgroups, s);
+    else launch_batch_pre_kw<1, MODE>(q, a, workgroups, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1555,7 +1634,11 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
         const int kw = plan.rows_per_wg / 16;
         a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
         a.n_quads = (batch + kQuad - 1) / kQuad;
-        launch_batch<kAdditive>(q, kw, a, plan.workgroups, s);
+        a.pre_bytes = pre_bytes(q, K, group, terms, exps, term_signs);
+        if (a.pre_bytes)
+            launch_batch_pre<kAdditive>(q, kw, a, plan.workgroups, s);
+        else
+            launch_batch<kAdditive>(q, kw, a, plan.workgroups, s);
         return launch_status();
     }
     RowsArgs a{};

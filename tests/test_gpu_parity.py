@@ -155,6 +155,9 @@ SMALL = [
     (1, 28672, 1152, 128, 5), (2, 28000, 256, 256, 8),
     # batch kernel, 64-row workgroups, eight quads
     (1, 28600, 256, 128, 32),
+    # batch kernel, every wave over 4, 8, 16 and 2 consecutive blocks
+    (3, 1000, 4096, 128, 4), (2, 300, 8192, 128, 16), (4, 100, 16384, 128, 3),
+    (1, 64, 2048, 128, 2),
     # generic kernel (any group % 8 == 0)
     (3, 100, 256, 8, 2), (1, 1, 8, 8, 1), (2, 257, 200, 40, 3), (3, 64, 1024, 64, 1),
     (4, 70, 96, 24, 1), (2, 33, 136, 136, 2),

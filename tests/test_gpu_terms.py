@@ -107,6 +107,14 @@ BATCH_CASES = [
     (2, 130, 384, 384, 5, 3, "ragged quad and rows"),
     (1, 77, 4224, 128, 6, 4, "ragged last piece"),
     (5, 300, 2048, 1024, 13, 2, "five planes, two pieces, ragged quad"),
+    # exponents and term signs preloaded per lane (G = 128, K % 1024 == 0)
+    (3, 1000, 4096, 128, 8, 2, "preloaded, 8 bytes"),
+    (2, 500, 8192, 128, 5, 2, "preloaded, 16 bytes"),
+    (3, 300, 4096, 128, 6, 4, "preloaded, 16 bytes, four terms"),
+    (1, 64, 2048, 128, 4, 4, "preloaded, 8 bytes, two pieces"),
+    (3, 200, 4096, 128, 4, 1, "preloaded, one term"),
+    (4, 300, 4096, 128, 8, 2, "four planes: per-piece loads"),
+    (3, 300, 4096, 128, 8, 3, "three terms: per-piece loads"),
 ]
 
 
@@ -130,6 +138,46 @@ def test_one_term_batch_matches_row_wise_batch_kernel():
                         N, K, G, B, yr)
     torch.cuda.synchronize()
     assert np.array_equal(y, yr.cpu().numpy().astype(np.float64))  # same arithmetic
+
+
+def test_one_term_batch_matches_row_wise_batch_kernel_preloaded():
+    """K = 4096: the additive kernel preloads its exponents and term signs,
+    the row-wise kernel loads them per piece; still the same arithmetic."""
+    q, N, K, G, B = 3, 1024, 4096, 128, 8
+    c = workloads.terms_case(q, N, K, G, B, 1, seed=13)
+    assert (c["term_signs"] != 0).all()
+    y = run(c)
+    yr = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm(dev(c["x"]), sa.pack_weights(dev(c["signs"])), dev(c["exps"][..., 0]), q,
+                        N, K, G, B, yr)
+    torch.cuda.synchronize()
+    assert np.array_equal(y, yr.cpu().numpy().astype(np.float64))
+
+
+@pytest.mark.parametrize("shift", [4, 8])
+def test_terms_batch_misaligned(shift):
+    """Exponents and term signs at addresses not aligned to the 16-byte preload
+    take the per-piece loads: the same arithmetic, so bit-identical output."""
+    q, N, K, G, B, T = 3, 700, 8192, 128, 6, 2
+    say(f"terms batch misaligned by {shift}")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=31)
+    y_al = run(c)
+
+    def shifted(a):
+        flat = torch.from_numpy(np.ascontiguousarray(a).reshape(-1)).cuda()
+        buf = torch.zeros(flat.numel() + 32, dtype=torch.int8, device="cuda")
+        view = buf[shift:shift + flat.numel()]
+        view.copy_(flat)
+        return view.view(a.shape)
+
+    y = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm_terms(dev(c["x"]), sa.pack_weights(dev(c["signs"])), shifted(c["exps"]),
+                              shifted(c["term_signs"]), q, N, K, G, T, B, y)
+    torch.cuda.synchronize()
+    y_mis = y.cpu().numpy().astype(np.float64)
+    assert np.array_equal(y_al, y_mis)
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G)
+    check(y_mis, y_ref, a_ref, "misaligned exponents and term signs")
 
 
 def test_terms_batch_full_size_sampled():
