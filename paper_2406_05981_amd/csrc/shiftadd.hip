@@ -868,6 +868,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     constexpr bool ADD = MODE == kAdditive;
     constexpr bool BLK = MODE == kBlockWise;
     constexpr bool COL = MODE == kColWise;
+    static_assert(!PRE || (ADD && Q <= 3), "preloaded exponents: additive mode, up to 3 planes");
     const int C = a.K >> 3, C16 = C >> 4, NG = a.K / a.G, bpg = a.G >> 7;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, p = lane >> 4;
@@ -908,12 +909,11 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
     const int8_t* exp_row = a.exps + (int64_t)n * NG;
 
     // PRE: bytes [pieces * wave * T, (pieces * wave + pieces) * T) of the row
-    constexpr int QP = PRE ? Q : 1, QS = (PRE && ADD) ? Q : 1;
+    constexpr int QP = PRE ? Q : 1, QS = PRE ? Q : 1;
     uint32_t pe[QP][4] = {}, ps[QS][4] = {};
     if constexpr (PRE) {
-        const int tb = ADD ? a.terms : 1;
-        const int64_t off0 = ((int64_t)n * NG + (int64_t)pieces * wave) * tb;
-        const int64_t plane = (int64_t)a.N * NG * tb;
+        const int64_t off0 = ((int64_t)n * NG + (int64_t)pieces * wave) * a.terms;
+        const int64_t plane = (int64_t)a.N * NG * a.terms;
         auto fetch = [&](const int8_t* src, uint32_t* w) {
             if (a.pre_bytes == 16) {
                 const uint4 v = *reinterpret_cast<const uint4*>(src);
@@ -928,12 +928,12 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
         for (int i = 0; i < Q; ++i) {
             fetch(a.exps + i * plane + off0, pe[i]);
-            if constexpr (ADD) fetch(a.term_signs + i * plane + off0, ps[QS > 1 ? i : 0]);
+            fetch(a.term_signs + i * plane + off0, ps[i]);
         }
     }
     // PRE: the T bytes of piece pc in a lane's preloaded words (T divides 4)
     auto pre_field = [&](const uint32_t* w, int pc) {
-        const int bo = pc * (ADD ? a.terms : 1);
+        const int bo = pc * a.terms;
         const int wi = bo >> 2;
         const uint32_t v = wi == 0 ? w[0] : wi == 1 ? w[1] : wi == 2 ? w[2] : w[3];
         return v >> (8 * (bo & 3));
@@ -1083,7 +1083,7 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
             } else if constexpr (ADD) {
                 if constexpr (PRE) {
                     j.et[i] = pre_field(pe[i], pc);
-                    j.st[i] = pre_field(ps[QS > 1 ? i : 0], pc);
+                    j.st[i] = pre_field(ps[i], pc);
                 }
                 asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
 #pragma unroll
@@ -1099,9 +1099,8 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                     }
                 }
             } else {
-                const int e = PRE ? (int)(int8_t)pre_field(pe[i], pc) : j.e[i];
 #pragma unroll
-                for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], e) * keep;
+                for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
             }
         }
     };
@@ -1400,14 +1399,13 @@ int pre_bytes(int q, int K, int G, int T, const void* p0, const void* p1) {
     return lw;
 }
 
+// q in [1, 3] (pre_bytes is 0 otherwise)
 template <int KW, int MODE>
 void launch_batch_pre_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
     const dim3 g(workgroups), b(kRowThreads);
-    switch (q) {
-        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, false, true>), g, b, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, false, true>), g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, false, true>), g, b, 0, s, a); break;
-    }
+    if (q == 1) hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, false, true>), g, b, 0, s, a);
+    else if (q == 2) hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, false, true>), g, b, 0, s, a);
+    else if (q == 3) hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, false, true>), g, b, 0, s, a);
 }
 
 template <int MODE>
@@ -1635,7 +1633,7 @@ SA_API int sa_shiftadd_gemm_terms(const uint16_t* x, const uint8_t* packed_bits,
         a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
         a.n_quads = (batch + kQuad - 1) / kQuad;
         a.pre_bytes = pre_bytes(q, K, group, terms, exps, term_signs);
-        if (a.pre_bytes)
+        if (a.pre_bytes && q <= 3)
             launch_batch_pre<kAdditive>(q, kw, a, plan.workgroups, s);
         else
             launch_batch<kAdditive>(q, kw, a, plan.workgroups, s);
