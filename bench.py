@@ -578,8 +578,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (--gpus {args.gpus} requested); "
-              "the layer shards along N across GPUs by design but no multi-GPU path is built",
+        print(f"bench.py: one GPU only (--gpus {args.gpus} requested): the layer shards "
+              "along N across GPUs by design, but no multi-GPU path is implemented",
               file=sys.stderr, flush=True)
         return 2
 

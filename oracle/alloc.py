@@ -18,7 +18,7 @@ What it computes (Sec. 4.3; parity is pinned by ``tests/test_alloc_oracle.py``):
 * ``allocate`` -- Eq. 4: one bit width per layer minimising sum_i C_{i,b_i}
   under sum_i b_i <= B L, by exhaustive enumeration (small L only).
 
-Readings where the paper is silent (each also stated in the design doc):
+Readings where the paper is silent:
 
 * X X^T is damped before the inverse: H = X X^T + damp * mean(diag(X X^T)) I,
   damp = 0.01 by default (the usual convention of the OBC/OPTQ line of work the

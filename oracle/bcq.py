@@ -27,7 +27,7 @@ factors of Sec. 4.1 (Eq. 2, one term):
   factor folded into the plane) and int8 exponents e_i = P_i, so that
   W_q = sum_i 2^{e_i} s_i per segment.
 
-Readings where the paper is silent (each also stated in the design doc):
+Readings where the paper is silent:
 
 * sign(0) = +1.
 * PoT is applied to the scales that BS uses (after every LS step) and to the
