@@ -1280,11 +1280,17 @@ void make_plan(int q, int N, int K, int group, int batch, sa_plan* p, int builds
         return;
     }
     const int groups = (N + kGroupRows - 1) / kGroupRows;
-    const int wgs = rows_workgroups(q, N);
+    int wgs = rows_workgroups(q, N);
+    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
+    // Several pieces and 449..512 row groups: two groups per workgroup on 225
+    // to 256 workgroups (16 waves, below), so each piece's tables serve 32
+    // rows instead of 16 (8192x28672 q=3: 27.2 -> 25.1 us); fewer groups would
+    // leave CUs idle
+    if (q <= kRowsResidentQ && p->pieces >= 2 && groups > 448 && groups <= 512)
+        wgs = (groups + 1) / 2;
     p->path = 1;
     p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);  // the largest share
     p->workgroups = wgs;
-    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
     // Two pieces in flight per workgroup (16 waves, 128 KB of tables) where
     // the workgroups leave a CU to each: up to 4 planes (128 registers at four
     // waves per SIMD), at most 256 workgroups, several pieces.
@@ -1303,11 +1309,12 @@ void make_plan_colwise(int q, int N, int K, int batch, sa_plan* p) {
     }
     *p = sa_plan{};
     const int groups = (N + kGroupRows - 1) / kGroupRows;
-    const int wgs = rows_workgroups(1, N);
+    int wgs = rows_workgroups(1, N);
+    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
+    if (p->pieces >= 2 && groups > 448 && groups <= 512) wgs = (groups + 1) / 2;  // as in make_plan
     p->path = 3;
     p->rows_per_wg = kGroupRows * ((groups + wgs - 1) / wgs);
     p->workgroups = wgs;
-    p->pieces = (K / 128 + kPieceBlocks - 1) / kPieceBlocks;
     const int split = (wgs <= 256 && p->pieces >= 2) ? 2 : 1;  // as in make_plan
     p->threads = kRowThreads * split;
     p->lds_bytes = sizeof(float) * split * (16 * kRegionFloats + kRowWaves * kGroupRows * kMaxRG);

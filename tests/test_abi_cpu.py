@@ -202,7 +202,11 @@ def test_colwise_validation_codes():
     assert sa.sa_plan_gemm(3, 4096, 11008, 128, 1)["threads"] == 1024
     assert sa.sa_plan_gemm(4, 3584, 8192, 128, 1)["threads"] == 1024
     assert sa.sa_plan_gemm(5, 4096, 11008, 128, 1)["threads"] == 512   # registers
-    assert sa.sa_plan_gemm(3, 8192, 28672, 128, 1)["threads"] == 512   # 512 workgroups
+    # 449..512 row groups and several pieces: two groups per workgroup, 16 waves
+    p = sa.sa_plan_gemm(3, 8192, 28672, 128, 1)
+    assert p["threads"] == 1024 and p["workgroups"] == 256 and p["rows_per_wg"] == 32
+    assert sa.sa_plan_gemm(3, 28672, 8192, 128, 1)["threads"] == 512   # 1792 groups
+    assert sa.sa_plan_gemm(3, 4200, 8320, 128, 1)["workgroups"] == 263  # 263 groups: one each
     assert sa.sa_plan_gemm(3, 4096, 4096, 128, 1)["threads"] == 512    # one piece
     assert sa.sa_plan_gemm_colwise(3, 4096, 11008, 1)["threads"] == 1024
     assert sa.sa_plan_gemm_blockwise(3, 4096, 11008, 512, 1)["threads"] == 1024

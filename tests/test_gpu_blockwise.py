@@ -63,6 +63,7 @@ CASES = [
     (5, 200, 1024, 2, 25, "five planes"),
     (3, 1000, 8320, 1, 125, "16 waves, three pieces, one-block last piece"),
     (2, 4096, 8192, 1, 512, "16 waves, 256 workgroups"),
+    (3, 8000, 8320, 1, 1000, "16 waves, two row groups per workgroup"),
     (4, 1000, 8320, 1, 125, "four planes: 8 waves"),
 ]
 

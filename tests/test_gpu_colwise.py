@@ -65,6 +65,7 @@ CASES = [
     (2, 1000, 2048, 16, "batch 16"),
     (3, 1000, 8320, 1, "16 waves, three pieces, one-block last piece"),
     (2, 4096, 8192, 1, "16 waves, 256 workgroups"),
+    (3, 8000, 8320, 1, "16 waves, two row groups per workgroup"),
 ]
 
 

@@ -145,6 +145,8 @@ SMALL = [
     # several pieces): odd piece count with a one-block last piece, 256
     # workgroups, one group spanning both pieces
     (4, 1000, 8320, 128, 1), (3, 4096, 12288, 256, 1), (1, 16, 8192, 8192, 1),
+    # ... with two row groups per workgroup (449..512 groups, several pieces)
+    (3, 8000, 8320, 128, 1), (2, 8192, 8192, 256, 1),
     # batch kernel (group % 128 == 0, batch >= 2), 16- and 32-row workgroups
     (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
     (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),

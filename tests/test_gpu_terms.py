@@ -62,6 +62,7 @@ CASES = [
     (3, 300, 4224, 128, 2, 4, "ragged last piece"),
     (3, 1000, 8320, 128, 1, 2, "16 waves, three pieces, one-block last piece"),
     (2, 4096, 8192, 256, 1, 3, "16 waves, 256 workgroups, G = 256"),
+    (3, 8000, 8320, 128, 1, 2, "16 waves, two row groups per workgroup"),
 ]
 
 
