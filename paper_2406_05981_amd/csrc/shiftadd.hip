@@ -651,13 +651,18 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     // loads makes the compiler copy registers at the loop back-edge, which
     // waits for every outstanding load and costs more than it hides.
     JobPos j{0, 0, 0, 0};
-    if (MODE == kRowWise && jobs == 1) {
+    // (additive: only when every workgroup has a single job; with one or two
+    // jobs per workgroup the general order below measured faster)
+    if ((MODE == kRowWise || (ADD && a.groups <= (int)gridDim.x)) && jobs == 1) {
         // A single job (a layer of at most 4096 columns and 16 rows per
         // workgroup): every request goes out at once, with no ordering
         // constraint, and the table build waits for the activations only.
         JobRegs<Q> regs;
         regs.xr = load_x(j);
-        load_job_exps<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
+        if constexpr (ADD)
+            load_job_terms<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
+        else
+            load_job_exps<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
         load_job_keys<Q>(a, row_of(j), block_of(j), C, 0, regs);
         __builtin_amdgcn_sched_barrier(0);
         build(regs.xr, regs.xe);
