@@ -1091,18 +1091,20 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                     j.st[i] = pre_field(ps[i], pc);
                 }
                 asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
+                // the plane's signed terms (sign -1, 0 or +1: the products are
+                // exact), then the piece's weight once
+                float pl[kQuad] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
                 for (int tt = 0; tt < kMaxTerms; ++tt) {
-                    const int sg = (int)(int8_t)(j.st[i] >> (8 * tt));
-                    if (tt < a.terms && sg != 0) {
+                    if (tt < a.terms) {
+                        const float sg = (float)(int8_t)(j.st[i] >> (8 * tt));
                         const int ex = (int)(int8_t)(j.et[i] >> (8 * tt));
 #pragma unroll
-                        for (int u = 0; u < kQuad; ++u) {
-                            const float v = ldexpf(s[u], ex) * keep;
-                            tot[u] += sg < 0 ? -v : v;
-                        }
+                        for (int u = 0; u < kQuad; ++u) pl[u] = fmaf(sg, ldexpf(s[u], ex), pl[u]);
                     }
                 }
+#pragma unroll
+                for (int u = 0; u < kQuad; ++u) tot[u] += pl[u] * keep;
             } else {
 #pragma unroll
                 for (int u = 0; u < kQuad; ++u) tot[u] += ldexpf(s[u], j.e[i]) * keep;
