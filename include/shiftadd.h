@@ -20,9 +20,9 @@
  * applied to each group's fp32 partial sum (ldexp), which equals shifting the
  * activations because the factor is constant over the group.
  *
- * Key convention (Sec. 4.1, "every eight grouped binary weights form an 8-bit
- * key"; the bit order is this library's reading): the key of chunk c of a plane
- * row is sum_{j<8} [s[8c+j] = +1] << j -- bit j stands for column 8c+j, a set
+ * Key convention (Sec. 4.1: the binary weights of one plane row are taken eight
+ * at a time as the index of a table; the bit order is this library's reading):
+ * the key of chunk c of a plane row is sum_{j<8} [s[8c+j] = +1] << j -- bit j stands for column 8c+j, a set
  * bit means +1.
  *
  * Conventions shared by every entry point:
@@ -100,8 +100,8 @@ SA_API int sa_pack_weights(const int8_t *signs, int q, int N, int K,
 SA_API int sa_unpack_weights(const uint8_t *packed_bits, int q, int N, int K,
                              int8_t *signs, void *stream);
 
-/* The tables of Sec. 4.1 ("pre-compute 256 possible values for every eight
- * elements"): for b < batch, c < K/8, m < 256,
+/* The tables of Sec. 4.1 (all 256 signed sums of each group of eight
+ * activations, computed before the queries): for b < batch, c < K/8, m < 256,
  *   lut[b][c][m] = sum_{j<8} (bit j of m ? +1 : -1) * x[b][8c+j]
  * computed in fp32 from the fp16 activations.  Entry m and entry 255-m are
  * exact negatives of each other.  This is the same construction the fused

@@ -8,8 +8,8 @@ The arithmetic lives in ``oracle.c`` (plain fp64 C, OpenMP over outputs); this
 module only builds and loads it and marshals numpy arrays.  What each function
 computes, with the passage it follows:
 
-* :func:`pack` / :func:`unpack` -- the 8-bit keys of Sec. 4.1 ("every eight
-  grouped binary weights form an 8-bit key"): byte c of a plane row is
+* :func:`pack` / :func:`unpack` -- the 8-bit keys of Sec. 4.1 (eight binary
+  weights of a plane row index one table): byte c of a plane row is
   ``sum_j [s[8c+j] > 0] << j``; bit value 1 stands for +1 (a reading: the paper
   does not fix the bit order or the bit-to-sign map).
 * :func:`lut` -- the 256 precomputed partial sums per 8 activations of Sec. 4.1:

@@ -6,7 +6,7 @@
 //   C  = ||IS||_F * STD(IS)^2
 //
 // computed as: the Gram matrix X X^T of fp16 calibration activations on the
-// matrix cores (v_mfma_f32_16x16x16_f16, fp32 accumulation; only the lower
+// matrix cores (v_mfma_f32_16x16x32_f16, fp32 accumulation; only the lower
 // triangle of tiles); the damped matrix in fp64 with rows and columns in reverse
 // order; a blocked fp64 Cholesky of it, because the diagonal of the Cholesky
 // factor of H^-1 is, in reverse order, the reciprocal of the diagonal of the

@@ -1092,13 +1092,16 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
                 }
                 asm volatile("" : "+v"(j.et[i]), "+v"(j.st[i]));
                 // the plane's signed terms (sign -1, 0 or +1: the products are
-                // exact), then the piece's weight once
+                // exact), then the piece's weight once.  A sign of 0 means no
+                // term, whatever its exponent byte holds: its shift is replaced
+                // by 0 (a select, no branch), so 0 * ldexp(s, 127) = 0 * inf
+                // can never turn the sum into NaN.
                 float pl[kQuad] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
                 for (int tt = 0; tt < kMaxTerms; ++tt) {
                     if (tt < a.terms) {
                         const float sg = (float)(int8_t)(j.st[i] >> (8 * tt));
-                        const int ex = (int)(int8_t)(j.et[i] >> (8 * tt));
+                        const int ex = sg != 0.0f ? (int)(int8_t)(j.et[i] >> (8 * tt)) : 0;
 #pragma unroll
                         for (int u = 0; u < kQuad; ++u) pl[u] = fmaf(sg, ldexpf(s[u], ex), pl[u]);
                     }

@@ -191,3 +191,21 @@ def test_terms_batch_full_size_sampled():
     y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G,
                                               rows=rows)
     check(y[:, rows], y_ref, a_ref, "4096x4096 batch 16 sampled")
+
+
+@pytest.mark.parametrize("B", [1, 2, 8])
+@pytest.mark.parametrize("K", [1024, 4096])
+def test_sign_zero_terms_ignore_their_exponent(B, K):
+    """A term sign of 0 means no term, whatever its exponent byte holds: with
+    every sign-0 term carrying exponent 127 (2^127 times a group sum overflows
+    fp32) the row kernel (batch 1) and the batch kernel (batch >= 2, per-piece
+    and preloaded exponents) still match the oracle, which skips such terms."""
+    q, N, G, T = 3, 300, 128, 3
+    say(f"sign-0 terms with exponent 127: K={K} B={B}")
+    c = workloads.terms_case(q, N, K, G, B, T, seed=41 + B + K)
+    zero = c["term_signs"] == 0
+    assert zero.any()
+    c["exps"][zero] = 127
+    y = run(c)
+    y_ref, a_ref = oracle.shiftadd_gemm_terms(c["x"], c["signs"], c["exps"], c["term_signs"], G)
+    check(y, y_ref, a_ref, f"sign-0 terms, exponent 127, batch {B}")
