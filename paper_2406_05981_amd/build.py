@@ -1,9 +1,13 @@
 """Compile the gfx950 HIP library ``libshiftadd.so`` in-tree with hipcc.
 
+Each source is compiled to an object in parallel, then the objects are linked
+into the shared library.
+
     python -m paper_2406_05981_amd.build
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import shutil
 import subprocess
@@ -25,21 +29,42 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def command(out: str = LIB, extra=()) -> list:
-    return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-            "-fvisibility=hidden", "-ffp-contract=off",
+def compile_flags(extra=()) -> list:
+    return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
+            "-ffp-contract=off",
             # packed fp32 VALU ops stay off: plain fp32 adds only
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-I", INCLUDE, *extra, "-o", out, *SOURCES]
+            "-I", INCLUDE, *extra]
+
+
+def command(out: str = LIB, extra=()) -> list:
+    """One hipcc command building the whole library from all sources."""
+    return [hipcc(), *compile_flags(extra), "-shared", "-o", out, *SOURCES]
 
 
 def build(verbose: bool = False) -> str:
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = command(tmp)
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    tag = f".tmp{os.getpid()}"
+    objs = [os.path.join(HERE, os.path.basename(src) + tag + ".o") for src in SOURCES]
+    cmds = [[hipcc(), *compile_flags(), "-c", "-o", obj, src] for src, obj in zip(SOURCES, objs)]
+    try:
+        with concurrent.futures.ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+            futs = []
+            for cmd in cmds:
+                if verbose:
+                    print(" ".join(cmd), flush=True)
+                futs.append(ex.submit(subprocess.run, cmd, check=True))
+            for f in futs:
+                f.result()
+        tmp = LIB + tag
+        link = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs]
+        if verbose:
+            print(" ".join(link), flush=True)
+        subprocess.run(link, check=True)
+        os.replace(tmp, LIB)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
     return LIB
 
 

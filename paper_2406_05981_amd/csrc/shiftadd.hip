@@ -390,7 +390,7 @@ constexpr bool kPipelineWords = Q <= 3 && !BLK;
 // term and added with the term's sign (0: no term).
 template <int Q, bool BLK = false>
 __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
-                                const uint32_t offs[2][4], const char* lut_bytes, int r = 0,
+                                const uint32_t offs[8], const char* lut_bytes, int r = 0,
                                 int terms = 0) {
     float tot = 0.0f;
 #pragma unroll
@@ -423,12 +423,16 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
             const uint32_t hi = (words[wd] & 0xf0f0f0f0u) | rgn_hi;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                // byte 0: slot offset (offs byte t); byte 1: row (byte t)
-                const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                // byte 0: slot offset (offs[2wd + t/2] byte t%2); byte 1:
+                // row (byte t); byte 2: the 64 KB half of the tables; the
+                // high halves sit 32 slots (128 bytes) further: the read's
+                // immediate offset
+                const uint32_t sel = 0x03020000u | ((4u + t) << 8) | (uint32_t)(t & 1);
+                const uint32_t o = offs[2 * wd + (t >> 1)];
                 Lo[t] = *reinterpret_cast<const float*>(
-                    lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
+                    lut_bytes + __builtin_amdgcn_perm(lo, o, sel));
                 Ho[t] = *reinterpret_cast<const float*>(
-                    lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
+                    lut_bytes + 128 + __builtin_amdgcn_perm(hi, o, sel));
             }
         };
         if constexpr (kPipelineWords<Q, BLK>) {
@@ -451,11 +455,12 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
                 const uint32_t hi = (words[wd] & 0xf0f0f0f0u) | rgn_hi;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const uint32_t sel = 0x0c0c0000u | ((4u + t) << 8) | (uint32_t)t;
+                    const uint32_t sel = 0x03020000u | ((4u + t) << 8) | (uint32_t)(t & 1);
+                    const uint32_t o = offs[2 * wd + (t >> 1)];
                     const float L = *reinterpret_cast<const float*>(
-                        lut_bytes + __builtin_amdgcn_perm(lo, offs[0][wd], sel));
+                        lut_bytes + __builtin_amdgcn_perm(lo, o, sel));
                     const float H = *reinterpret_cast<const float*>(
-                        lut_bytes + __builtin_amdgcn_perm(hi, offs[1][wd], sel));
+                        lut_bytes + 128 + __builtin_amdgcn_perm(hi, o, sel));
                     add_key(wd, t, L, H);
                 }
             }
@@ -509,17 +514,18 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
     const int planes = COL ? a.q : 1;
     const int jobs = a.B * planes * pieces * nrg;
 
-    // Slot offsets of this lane's 16 key positions, low and high half (4
-    // positions per register, one per byte): byte t of offs[h][wd] is 4*slot
-    // for position 4*wd+t, slot = 32*h + 16*(p & 1) + ((4*wd + t + r) & 15).
-    uint32_t offs[2][4];
+    // LDS address parts of this lane's 16 key positions, two positions per
+    // register: bytes 0 and 1 of offs[k] are 4*slot of positions 2k and
+    // 2k+1 (low half: slot = 16*(p & 1) + ((pos + r) & 15); the high half is
+    // 32 slots further), byte 2 is the 64 KB half of the tables this wave
+    // queries.  A query address is then one v_perm_b32 up to 128 KB, with no
+    // add for the second half.
+    uint32_t offs[8];
 #pragma unroll
-    for (int wd = 0; wd < 4; ++wd) {
-        // 4*((4*wd + t + r) & 15) for t = 0..3, one per byte
-        const uint32_t base4 = (uint32_t)(((4 * wd + r) & 15) * 4) * 0x01010101u;
-        const uint32_t steps = (base4 + 0x0c080400u) & 0x3c3c3c3cu;
-        offs[0][wd] = steps | (uint32_t)(64 * (p & 1)) * 0x01010101u;
-        offs[1][wd] = offs[0][wd] | 0x80808080u;
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t s0 = 16 * (p & 1) + ((2 * k + r) & 15);
+        const uint32_t s1 = 16 * (p & 1) + ((2 * k + 1 + r) & 15);
+        offs[k] = (4 * s0) | ((4 * s1) << 8) | ((uint32_t)half << 16);
     }
     const uint32_t rgn_lo = (uint32_t)((part >> 1) << 4) * 0x01010101u;
     const uint32_t rgn_hi = (uint32_t)(part >> 1) * 0x01010101u;
@@ -528,8 +534,10 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
 #pragma unroll
     for (int g = 0; g < kMaxRG; ++g) acc[g] = 0.0f;
 
-    lut += half * (16 * kRegionFloats);
+    // queries address all of the tables (the half is in the perm's byte 2);
+    // the build writes this half
     const char* lut_bytes = reinterpret_cast<const char*>(lut);
+    lut += half * (16 * kRegionFloats);
     // j.pc counts this half's pieces; the piece itself is H * j.pc + half
     auto row_of = [&](const JobPos& j) { return imin(kGroupRows * (rg0 + j.g) + r, a.N - 1); };
     auto block_of = [&](const JobPos& j) {
