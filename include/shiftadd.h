@@ -297,6 +297,18 @@ SA_API size_t sa_importance_workspace(void);
 SA_API int sa_importance_criterion(const float *w, int N, int K, const double *d, double *out,
                                    void *workspace, size_t workspace_bytes, void *stream);
 
+/* sa_importance_criterion for callers that cannot allocate (code under HIP
+ * graph capture, serving loops, harnesses that forbid allocation): the same
+ * kernels and result, with the partial sums in a fixed 16 KB device array the
+ * library owns (one per GPU, held until the process ends) instead of a
+ * workspace argument.  Calls no allocator.  The array is set up on the first
+ * call on each device (that device current).  Accepts the same sizes as
+ * sa_importance_criterion (N*K <= 2^40, else SA_ERR_SHAPE); out 8-byte
+ * aligned.  Calls that overlap on one GPU share the array and race: keep them
+ * on one stream. */
+SA_API int sa_importance_criterion_noalloc(const float *w, int N, int K, const double *d,
+                                           double *out, void *stream);
+
 /* Host only.  Per-bit estimates C_{i,b}: for each bit width (column b of
  * errors [L][nb], the measured reparameterization errors of L calibration
  * layers) the least-squares polynomial of the given degree in the criterion

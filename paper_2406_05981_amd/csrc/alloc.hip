@@ -15,6 +15,8 @@
 // bit totals, solved exactly on the host.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -423,6 +425,42 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
 
 SA_API size_t sa_importance_workspace(void) { return (size_t)2 * kStatBlocks * sizeof(double); }
 
+// The partial sums of sa_importance_criterion_noalloc: a fixed device array
+// (16 KB, one per GPU the library runs on, held until the process ends).  In
+// host code its name is only a stand-in for the symbol; the device address
+// comes from hipGetSymbolAddress, once per device, and only that address is
+// handed to kernels.
+static __device__ __align__(256) double scratch[2 * kStatBlocks];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+double* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of this device's `scratch` (the current device), or nullptr with
+// *status set when the runtime cannot provide it.
+double* scratch_on_current_device(int* status) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        *status = SA_ERR_HIP;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            *status = SA_ERR_HIP;
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = static_cast<double*>(p);
+    }
+    *status = SA_OK;
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
 SA_API int sa_importance_criterion(const float* w, int N, int K, const double* d, double* out,
                                    void* workspace, size_t workspace_bytes, void* stream) {
     if (!w || !d || !out || !workspace) return SA_ERR_NULL;
@@ -432,6 +470,23 @@ SA_API int sa_importance_criterion(const float* w, int N, int K, const double* d
         return SA_ERR_ALIGN;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     double* part = static_cast<double*>(workspace);
+    hipLaunchKernelGGL(k_is_partials, dim3(kStatBlocks), dim3(256), 0, s, w, N, K, d, part);
+    hipLaunchKernelGGL(k_is_final, dim3(1), dim3(256), 0, s, part, kStatBlocks, (int64_t)N * K,
+                       out);
+    return status();
+}
+
+SA_API int sa_importance_criterion_noalloc(const float* w, int N, int K, const double* d,
+                                           double* out, void* stream) {
+    if (!w || !d || !out) return SA_ERR_NULL;
+    if (N < 1 || K < 1 || (int64_t)N * K > ((int64_t)1 << 40)) return SA_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(out) & 7u) return SA_ERR_ALIGN;
+    int st = SA_OK;
+    double* part = scratch_on_current_device(&st);
+    if (!part) return st;
+    // the same kernels as sa_importance_criterion; every partial is written
+    // before it is read, so nothing needs clearing between calls
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(k_is_partials, dim3(kStatBlocks), dim3(256), 0, s, w, N, K, d, part);
     hipLaunchKernelGGL(k_is_final, dim3(1), dim3(256), 0, s, part, kStatBlocks, (int64_t)N * K,
                        out);

@@ -58,6 +58,7 @@ def _bind(lib):
         "sa_inverse_cholesky_diag": ([P, I, ctypes.c_double, P, P, ctypes.c_size_t, P], I),
         "sa_importance_workspace": ([], ctypes.c_size_t),
         "sa_importance_criterion": ([P, I, I, P, P, P, ctypes.c_size_t, P], I),
+        "sa_importance_criterion_noalloc": ([P, I, I, P, P, P], I),
         "sa_fit_per_bit": ([P, P, I, I, I, P], I),
         "sa_allocate_bits": ([P, P, I, I, ctypes.c_double, P, P], I),
         "sa_status_string": ([I], ctypes.c_char_p),
@@ -284,6 +285,15 @@ def sa_importance_criterion(w: torch.Tensor, N: int, K: int, d: torch.Tensor, ou
                                        _dev(workspace, "workspace", workspace.dtype,
                                             workspace.numel()), nbytes, _stream(stream)),
            "sa_importance_criterion")
+
+
+def sa_importance_criterion_noalloc(w: torch.Tensor, N: int, K: int, d: torch.Tensor,
+                                    out: torch.Tensor, stream=None) -> None:
+    _check(lib.sa_importance_criterion_noalloc(_dev(w, "w", torch.float32, N * K), N, K,
+                                               _dev(d, "d", torch.float64, K),
+                                               _dev(out, "out", torch.float64, 3),
+                                               _stream(stream)),
+           "sa_importance_criterion_noalloc")
 
 
 def sa_fit_per_bit(c, errors, degree: int = 1):
