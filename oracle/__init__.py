@@ -59,12 +59,28 @@ def build(force: bool = True) -> str:
     return _LIB_PATH
 
 
+def build_sanitized(out: str) -> str:
+    """Compile ``oracle.c`` with AddressSanitizer and UndefinedBehaviorSanitizer
+    (gcc) into ``out``; a process loading it must preload gcc's libasan.  Set
+    ``ORACLE_LIB`` to its path to make this module load it."""
+    tmp = out + f".tmp{os.getpid()}"
+    cmd = ["gcc", "-O1", "-g", "-fno-omit-frame-pointer", "-fopenmp", "-fPIC", "-shared",
+           "-std=c11", "-Wall", "-Wextra", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
 def _load():
     global _lib
     if _lib is not None:
         return _lib
-    build(force=False)
-    lib = ctypes.CDLL(_LIB_PATH)
+    path = os.environ.get("ORACLE_LIB")   # another build of oracle.c (the sanitized one)
+    if not path:
+        build(force=False)
+        path = _LIB_PATH
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     I64 = ctypes.c_int64
     lib.oracle_max_threads.argtypes = [ctypes.c_int]

@@ -68,6 +68,51 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def sanitized_flags() -> list:
+    """Host code under AddressSanitizer and UndefinedBehaviorSanitizer (each
+    -fsanitize= applies to the host pass only; device code is built as usual)."""
+    return ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host",
+            "-fno-omit-frame-pointer", "-shared-libsan"]
+
+
+def build_sanitized(out: str, verbose: bool = False) -> str:
+    """The library with its host code (validation, plans, the allocation fits and
+    dynamic programme) under ASan and UBSan, for the CPU tests; a process
+    loading it must preload clang's ASan runtime (``asan_runtime()``) and set
+    ``SHIFTADD_LIB`` to ``out``."""
+    tag = f".tmp{os.getpid()}"
+    objs = [out + "." + os.path.basename(src) + tag + ".o" for src in SOURCES]
+    flags = compile_flags(sanitized_flags())
+    cmds = [[hipcc(), *flags, "-c", "-o", obj, src] for src, obj in zip(SOURCES, objs)]
+    try:
+        with concurrent.futures.ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+            for f in [ex.submit(subprocess.run, cmd, check=True) for cmd in cmds]:
+                f.result()
+        tmp = out + tag
+        subprocess.run([hipcc(), f"--offload-arch={ARCH}", "-shared", *sanitized_flags(), "-o",
+                        tmp, *objs], check=True)
+        os.replace(tmp, out)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
+    return out
+
+
+def asan_runtime() -> str:
+    """Path of the clang ASan runtime the sanitized library links against."""
+    out = subprocess.run([hipcc(), "--print-file-name=libclang_rt.asan-x86_64.so"],
+                         capture_output=True, text=True).stdout.strip()
+    if out and os.path.isabs(out) and os.path.exists(out):
+        return out
+    import glob
+    found = sorted(glob.glob("/opt/rocm/lib/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not found:
+        raise RuntimeError("clang ASan runtime not found")
+    return found[-1]
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
     sys.exit(0)

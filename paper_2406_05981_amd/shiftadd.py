@@ -15,7 +15,9 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libshiftadd.so")
+# SHIFTADD_LIB selects another build of the same sources (the sanitized host
+# build of the CPU tests); by default the in-tree library
+LIB_PATH = os.environ.get("SHIFTADD_LIB") or os.path.join(_HERE, "libshiftadd.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
