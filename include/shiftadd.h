@@ -328,8 +328,8 @@ SA_API int sa_allocate_bits(const double *cost, const int *bits, int L, int nb, 
                             int *out, double *objective);
 
 /* Measurement aid, not part of the layer (no operation of the paper): reads
- * every byte of `buf` once -- each thread three 16-byte words, grid-strided, so
- * every wave request is 1 KiB of contiguous memory -- and writes at most one
+ * every byte of `buf` once -- each thread one 16-byte word, 256 threads per
+ * workgroup, so every wave request is 1 KiB of contiguous memory -- and writes at most one
  * float per wave into out[] (values unspecified).  Its time is that
  * of a plain read of `bytes` bytes, the practical floor a layer that streams as
  * many bytes is compared against.

@@ -1186,10 +1186,13 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_batch_wide(BatchArgs a) {
 // words of the buffer (grid-strided, so each request of a wave is 1 KiB of
 // contiguous memory) and folds them with xor, and each wave folds its lanes.
 // Its time is that of a plain read of the same bytes -- the practical floor a
-// layer streaming that many bytes is measured against.
+// layer streaming that many bytes is measured against.  The shape (256-thread
+// workgroups, one word per thread, as many workgroups as words / 256) was the
+// fastest of a sweep over 256, 512 and 1024 threads, 1 to 16 words per thread,
+// one-shot and persistent grids, at 6.7, 18 and 94 MB on gfx950.
 
-constexpr int kProbeThreads = 512;
-constexpr int kProbePer = 3;
+constexpr int kProbeThreads = 256;
+constexpr int kProbePer = 1;
 
 __global__ __launch_bounds__(kProbeThreads) void k_read_probe(const uint4* __restrict__ p,
                                                               int64_t n16, float* out) {
