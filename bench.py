@@ -518,7 +518,10 @@ def bench_criterion(args) -> int:
 
     us_gram = timed(gram, steps)
     us_all = timed(chain, steps)
-    tiles = (K // 128) * (K // 128 + 1) // 2  # 128 x 128 lower-triangular tiles
+    large = K >= 1024 and T >= 16384           # the library's large-shape Gram path
+    np_ = (K + 255) // 256
+    kernel = "k_gram_regions" if large else "k_gram_f16"
+    workgroups = np_ * np_ if large else (K // 128) * (K // 128 + 1) // 2
     flops_alg = K * (K + 1) * T          # the unique entries of X X^T, 2 flops per product
     tflops = flops_alg / us_gram / 1e6
     log(f"gram {us_gram:.1f} us ({tflops:.1f} TFLOP/s), whole criterion {us_all:.1f} us; "
@@ -538,7 +541,7 @@ def bench_criterion(args) -> int:
         "data": "synthetic (N(0,1) fp16 calibration activations with 1% outlier channels x20; "
                 "seeded fp32 weights)",
         "config": {"workload": f"criterion_{N}x{K}_T{T}", "N": N, "K": K, "tokens": T,
-                   "damp": 0.01, "kernel": "k_gram_f16", "gram_tiles": tiles},
+                   "damp": 0.01, "kernel": kernel, "gram_workgroups": workgroups},
         "gram_us": round(us_gram, 2),
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2),
                      "peak": F16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",

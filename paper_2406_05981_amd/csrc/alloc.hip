@@ -134,6 +134,349 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
             }
 }
 
+// ---------------------------------------------------------------- Gram matrix, large shapes
+//
+// For many calibration tokens the per-tile kernel above is bound by its own
+// operand traffic (a 128 x 128 tile reads 256 rows of X per 32 columns) and by
+// one wave per SIMD stalling on each stage.  The large-shape path works on
+// 256-row super-panels of X:
+//   * an off-diagonal 256 x 256 region of H (super-rows a > b) is split into
+//     two halves of the calibration columns, one workgroup each; the two fp32
+//     partials are added onto zero, which gives the same bits in either order;
+//   * a diagonal region (a, a) is one workgroup over all columns computing 8 of
+//     the 10 lower-triangle 64 x 64 quadrants; the other two, (3,2) and (3,3),
+//     are split over pieces of the columns (k_gram_rest) whose partials are
+//     kept in strictly-upper tiles of H and summed in piece order
+//     (k_gram_reduce);
+//   * finally the lower triangle is mirrored (k_gram_mirror).
+// With K = 4096 that is 256 equal workgroups, one per compute unit.  Operands
+// travel global -> LDS directly (16 bytes per lane, no register staging) into
+// a ring of four 32-column stages, two stages ahead of the one multiplied.
+
+constexpr int kGS = 256;       // super-panel rows
+constexpr int kGS2 = 32;       // calibration columns per stage (64-byte rows, 4 chunks)
+constexpr int kGRing = 4;      // LDS ring depth
+constexpr int kGPieces = 16;   // column pieces of each leftover quadrant pair
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte chunk c of LDS row r sits at chunk c ^ ((r >> 1) & 3): the operand
+// reads (16 consecutive rows, one chunk) and the 1 KB DMA blocks are both free
+// of bank conflicts (measured).
+__device__ inline int gswz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
+
+__device__ inline uint32_t lds_address(const void* p) {
+    return (uint32_t)(uintptr_t)((__attribute__((address_space(3))) const char*)(const char*)p);
+}
+// One global -> LDS load of 16 bytes per lane: lane l's bytes land at lds + 16 l.
+// M0 carries the LDS address; nothing else in these kernels uses M0.  The
+// compiler does not see these loads, so every wait on them is explicit.
+__device__ inline void dma16(const uint16_t* g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory");
+}
+template <int N>
+__device__ inline void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ inline void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// work item -> super-row a and r in [0, 2a]: r < 2a is half (r & 1) of the
+// off-diagonal region (a, r >> 1), r == 2a the diagonal region (a, a)
+__device__ inline void gram_item(int item, int& a, int& r) {
+    a = (int)sqrtf((float)item);
+    while ((a + 1) * (a + 1) <= item) ++a;
+    while (a * a > item) --a;
+    r = item - a * a;
+}
+
+// Eight waves.  Off-diagonal: wave w owns rows 128 (w >> 2) .. + 127 of the
+// A panel against rows 64 (w & 3) .. + 63 of the B panel (8 x 4 blocks of
+// 16 x 16).  Diagonal: wave w owns quadrant w of (0,0) (1,0) (1,1) (2,0)
+// (2,1) (2,2) (3,0) (3,1), both operands from the one panel.
+template <bool DIAG>
+__device__ inline void gram_region(const uint16_t* __restrict__ x, int K, int T, float* __restrict__ H,
+                                   int a, int bsr, int half, uint16_t* const* Ar, uint16_t* const* Br) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r16 = lane & 15, q = lane >> 4;
+    const int arow0 = kGS * a, brow0 = kGS * bsr;
+    constexpr int NDMA = DIAG ? 2 : 4;   // loads per wave per stage
+    const int S = T / kGS2;
+    const int sb = DIAG ? 0 : (half ? S / 2 : 0), se = DIAG ? S : (half ? S : S / 2);
+    // DMA rows of this wave: 32 w + 16 i + (lane >> 2), i < 2 (one 1 KB block per
+    // instruction); the swizzled chunk does not depend on i.  Rows past K read row K-1
+    // (their products only reach entries of H that are not written).
+    const int lrow = 32 * w + (lane >> 2);
+    const int chunk = gswz(lrow, lane & 3);
+    const uint16_t* pa0 = x + (int64_t)min(arow0 + lrow, K - 1) * T + 8 * chunk;
+    const uint16_t* pa1 = x + (int64_t)min(arow0 + lrow + 16, K - 1) * T + 8 * chunk;
+    const uint16_t* pb0 = x + (int64_t)min(brow0 + lrow, K - 1) * T + 8 * chunk;
+    const uint16_t* pb1 = x + (int64_t)min(brow0 + lrow + 16, K - 1) * T + 8 * chunk;
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    auto issue = [&](int st, int slot) __attribute__((always_inline)) {
+        const int t0 = st * kGS2;
+        const uint32_t la = lds_address(Ar[slot]) + (uint32_t)(32 * wu) * (kGS2 * 2);
+        dma16(pa0 + t0, la);
+        dma16(pa1 + t0, la + 16 * (kGS2 * 2));
+        if (!DIAG) {
+            const uint32_t lb = lds_address(Br[slot]) + (uint32_t)(32 * wu) * (kGS2 * 2);
+            dma16(pb0 + t0, lb);
+            dma16(pb1 + t0, lb + 16 * (kGS2 * 2));
+        }
+    };
+    constexpr int MU = DIAG ? 4 : 8, MV = 4;
+    int ra = 0, cb = 0;
+    if (DIAG) {
+        ra = w == 0 ? 0 : w <= 2 ? 1 : w <= 5 ? 2 : 3;
+        cb = w == 0 ? 0 : w <= 2 ? w - 1 : w <= 5 ? w - 3 : w - 6;
+    }
+    const int wr = DIAG ? 64 * ra : 128 * (w >> 2), wc = DIAG ? 64 * cb : 64 * (w & 3);
+    float4v acc[MU][MV];
+#pragma unroll
+    for (int u = 0; u < MU; ++u)
+#pragma unroll
+        for (int v = 0; v < MV; ++v) acc[u][v] = float4v{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](int slot) __attribute__((always_inline)) {
+        const uint16_t* Ab = Ar[slot];
+        const uint16_t* Bb = DIAG ? Ar[slot] : Br[slot];
+        half8 av[MU], bv[MV];
+#pragma unroll
+        for (int u = 0; u < MU; ++u) {
+            const int row = wr + 16 * u + r16;
+            av[u] = __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(Ab + row * kGS2 + 8 * gswz(row, q)));
+        }
+#pragma unroll
+        for (int v = 0; v < MV; ++v) {
+            const int row = wc + 16 * v + r16;
+            bv[v] = __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(Bb + row * kGS2 + 8 * gswz(row, q)));
+        }
+#pragma unroll
+        for (int u = 0; u < MU; ++u)
+#pragma unroll
+            for (int v = 0; v < MV; ++v)
+                acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[u], bv[v], acc[u][v], 0, 0, 0);
+    };
+    // Stage j sits in ring slot j % 4.  At stage j this wave's loads of stage j
+    // are waited for (those of j + 1 and j + 2 stay in flight), the workgroup
+    // meets (every wave's loads of j have landed, every wave is done with slot
+    // (j - 1) % 4), stage j + 3 is issued into that slot, and j is multiplied.
+    const int n = se - sb;
+    if (n > 0) issue(sb, 0);
+    if (n > 1) issue(sb + 1, 1);
+    if (n > 2) issue(sb + 2, 2);
+#define GRAM_STEP(j_, slot_)                                                             \
+    {                                                                                   \
+        const int j = (j_);                                                             \
+        if (j + 2 < n) wait_vmem<2 * NDMA>();                                           \
+        else if (j + 1 < n) wait_vmem<NDMA>();                                          \
+        else wait_vmem<0>();                                                            \
+        wg_barrier();                                                                   \
+        if (j + 3 < n) issue(sb + j + 3, ((slot_) + 3) % kGRing);                       \
+        compute(slot_);                                                                 \
+    }
+    int s = 0;
+    for (; s + kGRing <= n; s += kGRing) {
+        GRAM_STEP(s, 0);
+        GRAM_STEP(s + 1, 1);
+        GRAM_STEP(s + 2, 2);
+        GRAM_STEP(s + 3, 3);
+    }
+    if (s < n) GRAM_STEP(s, 0);
+    if (s + 1 < n) GRAM_STEP(s + 1, 1);
+    if (s + 2 < n) GRAM_STEP(s + 2, 2);
+#undef GRAM_STEP
+#pragma unroll
+    for (int u = 0; u < MU; ++u)
+#pragma unroll
+        for (int v = 0; v < MV; ++v)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int i = arow0 + wr + 16 * u + 4 * q + e;
+                const int j = (DIAG ? arow0 : brow0) + wc + 16 * v + r16;
+                if (i < K && j < K) {
+                    if (DIAG) H[(int64_t)i * K + j] = acc[u][v][e];
+                    else unsafeAtomicAdd(H + (int64_t)i * K + j, acc[u][v][e]);
+                }
+            }
+}
+
+__global__ __launch_bounds__(512) void k_gram_regions(const uint16_t* __restrict__ x, int K, int T,
+                                                      float* __restrict__ H, int n_items) {
+    __shared__ __attribute__((aligned(16))) uint16_t A0[kGS * kGS2], A1[kGS * kGS2], A2[kGS * kGS2], A3[kGS * kGS2];
+    __shared__ __attribute__((aligned(16))) uint16_t B0[kGS * kGS2], B1[kGS * kGS2], B2[kGS * kGS2], B3[kGS * kGS2];
+    uint16_t* const Ar[kGRing] = {A0, A1, A2, A3};
+    uint16_t* const Br[kGRing] = {B0, B1, B2, B3};
+    // workgroups are dealt round-robin over the 8 XCDs: give each XCD a
+    // contiguous run of items (neighbouring super-rows share panels in its L2)
+    const int b = blockIdx.x, qn = n_items / 8, rn = n_items % 8, xcd = b % 8;
+    const int item = xcd * qn + min(xcd, rn) + b / 8;
+    int a, r;
+    gram_item(item, a, r);
+    if (r == 2 * a) gram_region<true>(x, K, T, H, a, 0, 0, Ar, Br);
+    else gram_region<false>(x, K, T, H, a, r >> 1, r & 1, Ar, Br);
+}
+
+// Scratch slot m: 64 x 64 floats in quadrant (m % 4) of the (m / 4)-th strictly
+// upper 128 x 128 tile of H (row-major order of tiles); the large-shape path
+// writes nothing there before the final mirror.
+__device__ inline float* gram_slot(float* H, int K, int m) {
+    const int nt = K / 128;
+    int u = m >> 2, ti = 0;
+    while (u >= nt - 1 - ti) {
+        u -= nt - 1 - ti;
+        ++ti;
+    }
+    const int tj = ti + 1 + u;
+    return H + (int64_t)(128 * ti + 64 * ((m & 3) >> 1)) * K + 128 * tj + 64 * (m & 1);
+}
+
+// Quadrants (3,2) and (3,3) of diagonal region a (rows 192..255 of the region
+// against its rows 128..255) over piece p of the calibration columns; four
+// waves of 16 rows x 128 columns; partials to slots 2 (a P + p) and + 1.
+__global__ __launch_bounds__(256) void k_gram_rest(const uint16_t* __restrict__ x, int K, int T,
+                                                   float* __restrict__ H, int P) {
+    __shared__ __attribute__((aligned(16))) uint16_t A0[64 * kGS2], A1[64 * kGS2], A2[64 * kGS2], A3[64 * kGS2];
+    __shared__ __attribute__((aligned(16))) uint16_t B0[128 * kGS2], B1[128 * kGS2], B2[128 * kGS2], B3[128 * kGS2];
+    uint16_t* const Ar[kGRing] = {A0, A1, A2, A3};
+    uint16_t* const Br[kGRing] = {B0, B1, B2, B3};
+    const int a = blockIdx.x / P, p = blockIdx.x % P;
+    const int arow0 = kGS * a + 192, brow0 = kGS * a + 128;
+    const int S = T / kGS2;
+    const int sb = (int)((int64_t)S * p / P), se = (int)((int64_t)S * (p + 1) / P);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r16 = lane & 15, q = lane >> 4;
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    const int chunk = gswz(lane >> 2, lane & 3);
+    const uint16_t* pa = x + (int64_t)min(arow0 + 16 * w + (lane >> 2), K - 1) * T + 8 * chunk;
+    const uint16_t* pb0 = x + (int64_t)min(brow0 + 32 * w + (lane >> 2), K - 1) * T + 8 * chunk;
+    const uint16_t* pb1 = x + (int64_t)min(brow0 + 32 * w + 16 + (lane >> 2), K - 1) * T + 8 * chunk;
+    auto issue = [&](int st, int slot) __attribute__((always_inline)) {
+        const int t0 = st * kGS2;
+        dma16(pa + t0, lds_address(Ar[slot]) + (uint32_t)(16 * wu) * (kGS2 * 2));
+        dma16(pb0 + t0, lds_address(Br[slot]) + (uint32_t)(32 * wu) * (kGS2 * 2));
+        dma16(pb1 + t0, lds_address(Br[slot]) + (uint32_t)(32 * wu + 16) * (kGS2 * 2));
+    };
+    float4v acc[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) acc[v] = float4v{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](int slot) __attribute__((always_inline)) {
+        const int ra = 16 * w + r16;
+        const half8 av =
+            __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(Ar[slot] + ra * kGS2 + 8 * gswz(ra, q)));
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+            const int rb = 16 * v + r16;
+            const half8 bv =
+                __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(Br[slot] + rb * kGS2 + 8 * gswz(rb, q)));
+            acc[v] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bv, acc[v], 0, 0, 0);
+        }
+    };
+    constexpr int NDMA = 3;
+    const int n = se - sb;
+    if (n > 0) issue(sb, 0);
+    if (n > 1) issue(sb + 1, 1);
+    if (n > 2) issue(sb + 2, 2);
+#define GRAM_STEP(j_, slot_)                                                             \
+    {                                                                                   \
+        const int j = (j_);                                                             \
+        if (j + 2 < n) wait_vmem<2 * NDMA>();                                           \
+        else if (j + 1 < n) wait_vmem<NDMA>();                                          \
+        else wait_vmem<0>();                                                            \
+        wg_barrier();                                                                   \
+        if (j + 3 < n) issue(sb + j + 3, ((slot_) + 3) % kGRing);                       \
+        compute(slot_);                                                                 \
+    }
+    int s = 0;
+    for (; s + kGRing <= n; s += kGRing) {
+        GRAM_STEP(s, 0);
+        GRAM_STEP(s + 1, 1);
+        GRAM_STEP(s + 2, 2);
+        GRAM_STEP(s + 3, 3);
+    }
+    if (s < n) GRAM_STEP(s, 0);
+    if (s + 1 < n) GRAM_STEP(s + 1, 1);
+    if (s + 2 < n) GRAM_STEP(s + 2, 2);
+#undef GRAM_STEP
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        float* dst = gram_slot(H, K, 2 * (a * P + p) + k);
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dst[(int64_t)(16 * w + 4 * q + e) * K + 16 * v + r16] = acc[4 * k + v][e];
+    }
+}
+
+// The pieces of each leftover quadrant summed in piece order into H; workgroup =
+// (quadrant L, 16 of its rows).
+__global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ H, int K, int P) {
+    __shared__ float* src[kGPieces];
+    const int L = blockIdx.x >> 2, part = blockIdx.x & 3;
+    const int a = L >> 1, qd = L & 1;
+    if ((int)threadIdx.x < P) src[threadIdx.x] = gram_slot(H, K, 2 * (a * P + (int)threadIdx.x) + qd);
+    __syncthreads();
+    const int i0 = kGS * a + 192, j0 = kGS * a + 128 + 64 * qd;
+    for (int e = threadIdx.x; e < 16 * 64; e += 256) {
+        const int r = 16 * part + (e >> 6), c = e & 63;
+        float sum = 0.f;
+        for (int p = 0; p < P; ++p) sum += src[p][(int64_t)r * K + c];
+        if (i0 + r < K && j0 + c < K) H[(int64_t)(i0 + r) * K + j0 + c] = sum;
+    }
+}
+
+// H[i][j] = H[j][i] for i < j, one lower 64 x 64 tile (or diagonal tile) per workgroup.
+__global__ __launch_bounds__(256) void k_gram_mirror(float* __restrict__ H, int K) {
+    __shared__ float t[64][65];
+    const int b = blockIdx.x;
+    int ti = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
+    while ((ti + 1) * (ti + 2) / 2 <= b) ++ti;
+    while (ti * (ti + 1) / 2 > b) --ti;
+    const int tj = b - ti * (ti + 1) / 2;
+    const int i0 = 64 * ti, j0 = 64 * tj;
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int r = e >> 6, c = e & 63;
+        t[r][c] = H[(int64_t)(i0 + r) * K + j0 + c];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int r = e >> 6, c = e & 63;
+        const int di = j0 + r, dj = i0 + c;
+        if (di < dj) H[(int64_t)di * K + dj] = t[c][r];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0.f;
+}
+
+// The large-shape path pays five launches and one pass over H; it wins from
+// about 1024 channels and 16384 tokens (measured on the shapes in the tests).
+bool gram_large(int K, int T) { return K >= 1024 && T >= 16384; }
+
+int gram_large_launch(const uint16_t* x, int K, int T, float* H, hipStream_t s) {
+    const int np = (K + kGS - 1) / kGS;
+    const int n_items = np * np;
+    const int64_t kk = (int64_t)K * K;
+    const int zgrid = (int)((kk + 255) / 256 < 4096 ? (kk + 255) / 256 : 4096);
+    hipLaunchKernelGGL(k_fill_zero, dim3(zgrid), dim3(256), 0, s, H, kk);
+    hipLaunchKernelGGL(k_gram_regions, dim3(n_items), dim3(512), 0, s, x, K, T, H, n_items);
+    int n_diag = 0;   // diagonal regions whose quadrant row 3 holds channels
+    for (int a = 0; a < np; ++a)
+        if (kGS * a + 192 < K) ++n_diag;
+    if (n_diag) {
+        const int nt = K / 128;
+        const int slots = 2 * nt * (nt - 1);   // four per strictly upper 128 x 128 tile
+        int P = kGPieces;
+        if (P > slots / (2 * n_diag)) P = slots / (2 * n_diag);
+        if (P > T / kGS2) P = T / kGS2;
+        if (P < 1) return SA_ERR_SHAPE;
+        hipLaunchKernelGGL(k_gram_rest, dim3(n_diag * P), dim3(256), 0, s, x, K, T, H, P);
+        hipLaunchKernelGGL(k_gram_reduce, dim3(2 * n_diag * 4), dim3(256), 0, s, H, K, P);
+    }
+    const int n64 = K / 64;
+    hipLaunchKernelGGL(k_gram_mirror, dim3(n64 * (n64 + 1) / 2), dim3(256), 0, s, H, K);
+    return SA_OK;
+}
+
 // ---------------------------------------------------------------- damping, reversal
 
 // lambda = damp * mean(diag(H)) (fp64, one workgroup, fixed order).
@@ -384,9 +727,14 @@ SA_API int sa_gram_f16(const uint16_t* x, int K, int T, float* H, void* stream) 
         return SA_ERR_SHAPE;
     if ((reinterpret_cast<uintptr_t>(x) & 15u) || (reinterpret_cast<uintptr_t>(H) & 3u))
         return SA_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (gram_large(K, T)) {
+        const int rc = gram_large_launch(x, K, T, H, s);
+        if (rc != SA_OK) return rc;
+        return status();
+    }
     const int tiles = K / kGT;
-    hipLaunchKernelGGL(k_gram_f16, dim3(tiles * (tiles + 1) / 2), dim3(256), 0,
-                       reinterpret_cast<hipStream_t>(stream), x, K, T, H);
+    hipLaunchKernelGGL(k_gram_f16, dim3(tiles * (tiles + 1) / 2), dim3(256), 0, s, x, K, T, H);
     return status();
 }
 

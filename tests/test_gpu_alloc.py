@@ -57,7 +57,10 @@ def gpu_d(H, damp):
     return d.cpu().numpy()
 
 
-@pytest.mark.parametrize("K,T", [(128, 32), (128, 96), (256, 512), (512, 2048), (1024, 160)])
+@pytest.mark.parametrize("K,T", [(128, 32), (128, 96), (256, 512), (512, 2048), (1024, 160),
+                                 # the large-shape path (K >= 1024, T >= 16384): whole super-panels,
+                                 # a half-empty last super-panel (K % 256 == 128), T an odd multiple of 32
+                                 (1024, 16384), (1152, 16416)])
 def test_gram(K, T):
     say(f"gram K={K} T={T}")
     x = calib(K, T, seed=K + T)
@@ -67,6 +70,21 @@ def test_gram(K, T):
     bound = 2 * T * 2.0 ** -24 * (np.abs(x64) @ np.abs(x64).T)
     assert (np.abs(H - ref) <= bound).all()
     assert np.array_equal(H, H.T)
+
+
+@pytest.mark.parametrize("K,T", [(128, 96), (1152, 16416)])
+def test_gram_repeatable(K, T):
+    """Two calls give the same bits (the large-shape path adds exactly two
+    partials onto zero per entry, and sums the column pieces of the leftover
+    quadrants in a fixed order)."""
+    say(f"gram repeatable K={K} T={T}")
+    x = torch.from_numpy(calib(K, T, seed=7)).cuda()
+    H1 = torch.empty((K, K), dtype=torch.float32, device="cuda")
+    H2 = torch.full((K, K), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_gram_f16(x, K, T, H1)
+    sa.sa_gram_f16(x, K, T, H2)
+    torch.cuda.synchronize()
+    assert torch.equal(H1, H2)
 
 
 @pytest.mark.parametrize("K,T,damp", [(64, 256, 0.01), (200, 512, 0.01), (384, 256, 0.05),
@@ -100,7 +118,8 @@ def test_criterion_from_d():
     assert o[2] == pytest.approx(IS.std(), rel=1e-12)
 
 
-@pytest.mark.parametrize("N,K,T", [(128, 128, 1024), (1024, 1024, 4096), (4096, 2048, 8192)])
+@pytest.mark.parametrize("N,K,T", [(128, 128, 1024), (1024, 1024, 4096), (4096, 2048, 8192),
+                                   (512, 1024, 16384)])
 def test_criterion_end_to_end(N, K, T):
     """Eq. 3 for one layer from its weights and fp16 calibration activations;
     the largest case is a 2048-channel layer with 8192 calibration tokens."""
