@@ -181,13 +181,43 @@ __device__ inline void wait_vmem() {
 }
 __device__ inline void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// work item -> super-row a and r in [0, 2a]: r < 2a is half (r & 1) of the
-// off-diagonal region (a, r >> 1), r == 2a the diagonal region (a, a)
-__device__ inline void gram_item(int item, int& a, int& r) {
-    a = (int)sqrtf((float)item);
-    while ((a + 1) * (a + 1) <= item) ++a;
-    while (a * a > item) --a;
-    r = item - a * a;
+// Work item li -> region: first the first halves of all off-diagonal regions
+// (a > b), then the diagonal regions, then the second halves.  Off-diagonal
+// regions are listed in blocks of 4 super-rows x 8 super-columns, so the 32
+// consecutive items one XCD receives share few panels of X at one position in
+// the calibration columns (its L2 serves them all).
+__device__ inline void gram_offdiag(int idx, int np, int& a, int& b) {
+    for (int a0 = 0; a0 < np; a0 += 4) {
+        const int a1 = min(np, a0 + 4);
+        for (int b0 = 0; b0 < a1 - 1; b0 += 8) {
+            const int b1 = b0 + 8;
+            int cnt = 0;
+            for (int x = a0; x < a1; ++x) cnt += max(0, min(b1, x) - b0);
+            if (idx < cnt) {
+                for (int x = a0; x < a1; ++x) {
+                    const int k = max(0, min(b1, x) - b0);
+                    if (idx < k) {
+                        a = x;
+                        b = b0 + idx;
+                        return;
+                    }
+                    idx -= k;
+                }
+            }
+            idx -= cnt;
+        }
+    }
+    a = b = 0;
+}
+__device__ inline void gram_region_of(int li, int np, int& a, int& b, int& half, bool& diag) {
+    const int n_off = np * (np - 1) / 2;
+    diag = li >= n_off && li < n_off + np;
+    half = li >= n_off + np ? 1 : 0;
+    if (diag) {
+        a = b = li - n_off;
+        return;
+    }
+    gram_offdiag(half ? li - n_off - np : li, np, a, b);
 }
 
 // Eight waves.  Off-diagonal: wave w owns rows 128 (w >> 2) .. + 127 of the
@@ -310,10 +340,13 @@ __global__ __launch_bounds__(512) void k_gram_regions(const uint16_t* __restrict
     // contiguous run of items (neighbouring super-rows share panels in its L2)
     const int b = blockIdx.x, qn = n_items / 8, rn = n_items % 8, xcd = b % 8;
     const int item = xcd * qn + min(xcd, rn) + b / 8;
-    int a, r;
-    gram_item(item, a, r);
-    if (r == 2 * a) gram_region<true>(x, K, T, H, a, 0, 0, Ar, Br);
-    else gram_region<false>(x, K, T, H, a, r >> 1, r & 1, Ar, Br);
+    int np = 1;
+    while (np * np < n_items) ++np;
+    int a, bsr, half;
+    bool diag;
+    gram_region_of(item, np, a, bsr, half, diag);
+    if (diag) gram_region<true>(x, K, T, H, a, 0, 0, Ar, Br);
+    else gram_region<false>(x, K, T, H, a, bsr, half, Ar, Br);
 }
 
 // Scratch slot m: 64 x 64 floats in quadrant (m % 4) of the (m / 4)-th strictly
