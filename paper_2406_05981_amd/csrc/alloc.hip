@@ -568,8 +568,8 @@ __device__ inline void cfor(F&& f) {
     }
 }
 
-__global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K, int j) {
-    const int r = threadIdx.x;
+// One wave (lane r = row r of the block).
+__device__ __attribute__((always_inline)) inline void chol_crout(double* __restrict__ A, int K, int j, int r) {
     const int nb = min(kNB, K - j);
     double a[kNB];
     cfor<0, kNB>([&](auto c_) {
@@ -598,6 +598,12 @@ __global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K,
         constexpr int c = decltype(c_)::value;
         if (r < nb && c < nb && c <= r) A[(int64_t)(j + r) * K + j + c] = a[c];
     });
+}
+
+// The first diagonal block; later ones are factored by the trailing update
+// that finishes them (k_chol_syrk).
+__global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K, int j) {
+    chol_crout(A, K, j, threadIdx.x);
 }
 
 // Panel below the diagonal block: row r (r >= j + 64) solves x L11^T = a, one
@@ -676,6 +682,14 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
             const int r = r0 + rr + u, s = s0 + ss + v;
             if (r < K && s < K && s <= r) A[(int64_t)r * K + s] -= acc[u][v];
         }
+    // Tile (0, 0) is the next panel's diagonal block, final once this tile is
+    // written: its first wave factors it while the other tiles are still being
+    // updated (one launch per panel fewer, and the factorization off the
+    // critical path wherever the update takes longer than it).
+    if (b == 0) {
+        __syncthreads();
+        if (threadIdx.x < 64) chol_crout(A, K, base, (int)threadIdx.x);
+    }
 }
 
 // d[k] = 1 / L[K-1-k][K-1-k]: the diagonal of the Cholesky factor of H^-1.
@@ -791,8 +805,8 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
     const int64_t n = (int64_t)K * K;
     const int grid = (int)(((n + 255) / 256) < 8192 ? (n + 255) / 256 : 8192);
     hipLaunchKernelGGL(k_reverse, dim3(grid), dim3(256), 0, s, H, K, lambda, A);
+    hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(64), 0, s, A, K, 0);
     for (int j = 0; j < K; j += kNB) {
-        hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(64), 0, s, A, K, j);
         const int below = K - j - kNB;
         if (below > 0) {
             const int rb = (below + kNB - 1) / kNB;
