@@ -640,7 +640,7 @@ __global__ __launch_bounds__(64) void k_chol_trsm(double* __restrict__ A, int K,
 
 // Trailing update of the lower triangle: A[r][s] -= sum_c L[r][c] L[s][c] over
 // the panel's 64 columns, for 64 x 64 tiles (tr >= ts) below the panel.  Each
-// thread owns a 4 x 4 block of the tile.
+// thread owns 4 x 4 entries of the tile.
 __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K, int j) {
     __shared__ double lr_[kNB * kNBP];
     __shared__ double ls_[kNB * kNBP];
@@ -657,7 +657,10 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
         ls_[r * kNBP + c] = s0 + r < K ? A[(int64_t)(s0 + r) * K + j + c] : 0.0;
     }
     __syncthreads();
-    const int rr = (threadIdx.x >> 4) * 4, ss = (threadIdx.x & 15) * 4;
+    // thread (ty, tx) owns rows ty + 16 u and columns tx + 16 v: the 16 lanes of
+    // a read cover 16 consecutive rows (no bank conflicts with the 65-double
+    // stride) and the update writes 128-byte runs
+    const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
     double acc[4][4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
@@ -667,8 +670,8 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
         double a4[4], b4[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            a4[u] = lr_[(rr + u) * kNBP + c];
-            b4[u] = ls_[(ss + u) * kNBP + c];
+            a4[u] = lr_[(ty + 16 * u) * kNBP + c];
+            b4[u] = ls_[(tx + 16 * u) * kNBP + c];
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
@@ -679,7 +682,7 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
     for (int u = 0; u < 4; ++u)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int r = r0 + rr + u, s = s0 + ss + v;
+            const int r = r0 + ty + 16 * u, s = s0 + tx + 16 * v;
             if (r < K && s < K && s <= r) A[(int64_t)r * K + s] -= acc[u][v];
         }
     // Tile (0, 0) is the next panel's diagonal block, final once this tile is
