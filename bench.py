@@ -55,7 +55,7 @@ def source_hash() -> str:
 # row kernel (path 1) or the batch kernel (path 2) in its additive mode
 KERNELS = {0: "k_gemm_generic", 1: "k_gemm_rows", 2: "k_gemm_batch", 3: "k_gemm_rows_col",
            4: "k_gemm_rows_blk", 5: "k_gemm_batch_blk", 6: "k_gemm_batch_col", "add1": "k_gemm_rows_add",
-           "add2": "k_gemm_batch_add"}
+           "add2": "k_gemm_batch_add", "kslice": "k_gemm_kslice"}
 
 
 def measured_traffic(kernel: str, workload: str, layer: int, batch: int):
@@ -593,6 +593,9 @@ def main() -> int:
     ap.add_argument("--colwise", action="store_true",
                     help="the layer with column-wise factors (sa_shiftadd_gemm_colwise) on the "
                          "workload layer's shape")
+    ap.add_argument("--kslice", action="store_true",
+                    help="batch 1, row-wise: the whole-table form (1024-column K slices, "
+                         "sa_shiftadd_gemm_kslice)")
     ap.add_argument("--blockwise", action="store_true",
                     help="the layer with block-wise factors (sa_shiftadd_gemm_blockwise, blocks "
                          "of 8 columns x N/8 rows) on the workload layer's shape")
@@ -680,9 +683,18 @@ def main() -> int:
         bytes_step = algorithmic_bytes(q, N, K, G, B)
         weight_bytes = q * N * K // 8 + q * N * (K // G)
         plan = sa.sa_plan_gemm(q, N, K, G, B)
+        if args.kslice:
+            if B != 1 or K % 1024 or G % 128:
+                log("--kslice needs batch 1, K % 1024 == 0 and group % 128 == 0")
+                return 2
+            slices = K // 1024
+            ranges = max(1, min(256 // slices, -(-(-(-N // 8)) // 16)))
+            plan = {"path": "kslice", "rows_per_wg": -(-N // ranges), "workgroups": slices * ranges,
+                    "threads": 1024, "pieces": 1, "lds_bytes": 131072}
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / weight_bytes))
     mode = (" column-wise" if colwise else " block-wise" if blockwise else
-            f" additive, {terms} terms" if terms else "")
+            f" additive, {terms} terms" if terms else " whole tables, K slices" if args.kslice
+            else "")
     log(f"workload {args.workload}/{L.name}{mode}: q={q} N={N} "
         f"K={K} G={G} B={B}; {copies} weight copies ({copies * weight_bytes / 1e6:.0f} MB); "
         f"plan {plan}")
@@ -720,6 +732,8 @@ def main() -> int:
             del d
     x = torch.from_numpy(d0["x"]).cuda()
     y = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    ws = (torch.empty(sa.sa_kslice_workspace_bytes(N, K) // 4, dtype=torch.float32, device="cuda")
+          if args.kslice else None)
     torch.cuda.synchronize()
     log(f"inputs generated and packed in {time.perf_counter() - t0:.1f} s")
 
@@ -733,6 +747,8 @@ def main() -> int:
             sa.sa_shiftadd_gemm_blockwise(x, packed[c], exps[c], q, N, K, rb, B, y)
         elif colwise:
             sa.sa_shiftadd_gemm_colwise(x, packed[c], exps[c], q, N, K, B, y)
+        elif args.kslice:
+            sa.sa_shiftadd_gemm_kslice(x, packed[c], exps[c], q, N, K, G, y, ws)
         else:
             sa.sa_shiftadd_gemm(x, packed[c], exps[c], q, N, K, G, B, y)
 
@@ -807,6 +823,9 @@ def main() -> int:
             "workload": args.workload,
             "layer": L.name,
             "N": N, "K": K, "q": q, "group": None if colwise or blockwise else G, "batch": B,
+            "tables": ("256 entries per chunk, 1024-column K slices, partials added in slice "
+                       "order by a second kernel" if args.kslice else
+                       "factored 16-entry halves per chunk"),
             "scales": ("column-wise (one exponent per plane and column)" if colwise else
                        f"block-wise (8 columns x {rb} rows)" if blockwise else
                        f"row-wise, group {G}, additive, {terms} terms" if terms else

@@ -130,6 +130,25 @@ SA_API int sa_build_lut(const uint16_t *x, int K, int batch, float *lut, void *s
 SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
                             int q, int N, int K, int group, int batch, float *y, void *stream);
 
+/* The same layer at batch 1 with the whole 256-entry table of every chunk
+ * (Sec. 4.1), one LDS read and one add per key.  K is cut into 1024-column
+ * slices; a workgroup builds the 128 chunk tables of one slice once and
+ * streams a range of rows through them, writing one fp32 partial per (slice,
+ * row) to `workspace`; a second kernel adds each row's partials in slice
+ * order into y.  Arguments as for sa_shiftadd_gemm with batch = 1, and:
+ *   K % 1024 == 0 and group % 128 == 0 (else SA_ERR_SHAPE, SA_ERR_GROUP);
+ *   workspace        (device) fp32, at least sa_kslice_workspace_bytes(N, K)
+ *                    bytes = 4 * (K / 1024) * N (else SA_ERR_SHAPE; NULL:
+ *                    SA_ERR_NULL); owned by the caller, overwritten; calls
+ *                    that share a workspace must not overlap.
+ * Deterministic; y is bit-identical across calls but not to sa_shiftadd_gemm
+ * (a different fp32 summation order).  Allocates nothing; may be captured in
+ * a HIP graph. */
+SA_API size_t sa_kslice_workspace_bytes(int N, int K);
+SA_API int sa_shiftadd_gemm_kslice(const uint16_t *x, const uint8_t *packed_bits,
+                                   const int8_t *exps, int q, int N, int K, int group, float *y,
+                                   float *workspace, size_t workspace_bytes, void *stream);
+
 /* The offline reparameterization that produces the layer's planes and
  * exponents from full-precision weights: alternating multi-bit binary-coding
  * quantization (Sec. 3, Alg. 1: greedy initialisation on residuals, Eq. 1, then

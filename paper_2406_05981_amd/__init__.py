@@ -13,7 +13,8 @@ __all__ = [
     "sa_plan_gemm_blockwise", "shiftadd_gemm_blockwise", "sa_shiftadd_gemm_terms",
     "sa_quantize_bcq_terms", "quantize_bcq_terms", "sa_gram_f16", "sa_inverse_cholesky_diag",
     "sa_importance_criterion", "sa_fit_per_bit", "sa_allocate_bits", "bit_criterion",
-    "pack_weights", "shiftadd_gemm", "SaError",
+    "pack_weights", "shiftadd_gemm", "SaError", "sa_shiftadd_gemm_kslice",
+    "sa_kslice_workspace_bytes",
 ]
 
 

@@ -773,6 +773,188 @@ __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_add_wide(RowsArgs a) 
     gemm_rows_body<Q, 1, kAdditive>(a, lut, red);
 }
 
+// ---------------------------------------------------------------- K-slice kernel with full tables
+//
+// Row-wise factors, batch 1.  The 256-entry table of each chunk (Sec. 4.1) is
+// stored whole, so a query is one LDS read and one add per key instead of two
+// of each.  Rebuilding 256 entries per chunk for every piece of a row kernel
+// costs more LDS time than the halved reads save (LDS writes cost about twice
+// what reads do on gfx950), so here a workgroup owns one 1024-column slice of
+// K, builds its 128 KB of tables once, and streams every row of its row range
+// through them.  Each workgroup writes one fp32 partial per (slice, row) to a
+// workspace; a second kernel adds the slices of a row in slice order
+// (deterministic).
+//
+// LDS layout (128 chunks): half h (chunks 64h..64h+63) holds 256 rows of 64
+// four-byte slots, entry m of chunk 64h + s at float h*16384 + m*64 + s.  The
+// bank of a read is its slot alone, whatever the key, so a query address is
+// one v_perm_b32 (byte 0 = 4*slot, byte 1 = the key byte itself, byte 2 = h),
+// and a half-wave's reads are conflict-free when its 32 lanes ask for 32
+// different chunks.
+//
+// Build: thread t writes the 32 entries of chunk 64*((t >> 6) & 1) + (t & 63)
+// whose high nibble is 2*(t >> 7) or 2*(t >> 7) + 1, entry m = lo[m & 15] +
+// hi[m >> 4] with the nibble sums of the row kernel (entries m and 255 - m
+// are exact negatives).  A wave's writes of one entry fill one 256-byte row.
+//
+// Queries: a job is 8 consecutive rows (starting at a multiple of 8) of the
+// slice; lane (r = lane & 7, b = lane >> 3) of the wave owns row r, block b
+// (blocks 0-3 in half 0, 4-7 in half 1).  Keys are stored rotated by row
+// (position t of a row's 16 bytes holds chunk (t + row) mod 16), so the 8
+// rows x 4 blocks of a half-wave ask for 32 different chunks.  Wave w takes
+// jobs w, w + 16, ... of its range; every job of a wave has the same row
+// parity, so the lane's slot offsets are fixed.  The next job's keys and
+// exponents are requested before the current job's queries.
+constexpr int kSliceBlocks = 8;                             // 1024 columns per slice
+constexpr int kSliceCols = kSliceBlocks * 128;
+constexpr int kSliceHalfFloats = 256 * 64;                  // 64 KB
+constexpr int kSliceThreads = 1024;                         // 16 waves
+constexpr int kSliceWaves = kSliceThreads / 64;
+constexpr int kSliceJobRows = 8;
+
+struct SliceArgs {
+    const uint16_t* x;
+    const uint8_t* packed;
+    const int8_t* exps;
+    int q, N, K, G;
+    int slices, ranges;  // grid = slices * ranges
+    int jobs;            // ceil(N / 8)
+    float* part;         // [slices][N]
+};
+
+template <int Q>
+struct SliceRegs {
+    uint4 w[Q];
+    int e[Q];  // exponent, sign-extended by the load
+};
+
+template <int Q>
+__global__ __launch_bounds__(kSliceThreads) void k_gemm_kslice(SliceArgs a) {
+    __shared__ float tab[2 * kSliceHalfFloats];
+    const int C = a.K >> 3, NG = a.K / a.G, bpg = a.G >> 7;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int slice = (int)blockIdx.x % a.slices, range = (int)blockIdx.x / a.slices;
+    // jobs [j0, j1) of this range, spread evenly over the ranges
+    const int jbase = a.jobs / a.ranges, jextra = a.jobs - jbase * a.ranges;
+    const int j0 = range * jbase + imin(range, jextra);
+    const int j1 = j0 + jbase + (range < jextra ? 1 : 0);
+    const int nj = j1 - j0 > wave ? (j1 - j0 - wave + kSliceWaves - 1) / kSliceWaves : 0;
+
+    const int r = lane & 7, b = lane >> 3;
+    const int rr = r + 8 * ((j0 + wave) & 1);  // row mod 16 of this lane's rows
+    const int J = kSliceBlocks * slice + b;    // block of the whole row
+    uint32_t offs[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t s0 = 16 * (b & 3) + ((2 * k + rr) & 15);
+        const uint32_t s1 = 16 * (b & 3) + ((2 * k + 1 + rr) & 15);
+        offs[k] = (4 * s0) | ((4 * s1) << 8) | ((uint32_t)(b >> 2) << 16);
+    }
+    const char* tab_bytes = reinterpret_cast<const char*>(tab);
+
+    auto row_of = [&](int k) {  // row of this lane in the wave's k-th job (clamped)
+        const int n = kSliceJobRows * (j0 + wave + kSliceWaves * imin(k, nj - 1)) + r;
+        return n < 0 ? 0 : imin(n, a.N - 1);
+    };
+    auto load_job = [&](int k, SliceRegs<Q>& g) {
+        const int n = row_of(k);
+        const uint32_t eoff = (uint32_t)(n * NG + (bpg == 1 ? J : J / bpg));
+#pragma unroll
+        for (int i = 0; i < Q; ++i) g.e[i] = (a.exps + (size_t)i * a.N * NG)[eoff];
+        const int T = n >> 6;
+        const int R = imin(kTileRows, a.N - kTileRows * T);
+        const uint32_t off = (uint32_t)(kTileRows * T * C + 16 * (n & 63) + kBlockChunks * J * R);
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+            g.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)i * a.N * C + off);
+    };
+    // queries of one job, then the row's 8 blocks combined in a fixed order
+    auto run_job = [&](int k, SliceRegs<Q>& g) {
+        float tot = 0.0f;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            const uint32_t words[4] = {g.w[i].x, g.w[i].y, g.w[i].z, g.w[i].w};
+            float s = 0.0f;
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t sel = 0x03020000u | ((4u + t) << 8) | (uint32_t)(t & 1);
+                    const float v = *reinterpret_cast<const float*>(
+                        tab_bytes + __builtin_amdgcn_perm(words[wd], offs[2 * wd + (t >> 1)], sel));
+                    s = (wd == 0 && t == 0) ? v : s + v;
+                }
+            }
+            tot += ldexpf(s, g.e[i]);
+        }
+        tot += __shfl_xor(tot, 8);
+        tot += __shfl_xor(tot, 16);
+        tot += __shfl_xor(tot, 32);
+        const int n = kSliceJobRows * (j0 + wave + kSliceWaves * k) + r;
+        if (lane < kSliceJobRows && k < nj && n < a.N) a.part[(size_t)slice * a.N + n] = tot;
+    };
+
+    // the slice's tables, built once: activations requested first, then the
+    // first job's keys, so the build waits for the activations only
+    const int slot = threadIdx.x & 63, half = (threadIdx.x >> 6) & 1, kq = threadIdx.x >> 7;
+    const uint4 xr = *reinterpret_cast<const uint4*>(a.x + kSliceCols * slice +
+                                                     8 * (64 * half + slot));
+    __builtin_amdgcn_sched_barrier(0);
+    SliceRegs<Q> ga, gb;
+    load_job(0, ga);  // (a valid row even for a wave without jobs)
+    __builtin_amdgcn_sched_barrier(0);
+    {
+        const uint32_t w4[4] = {xr.x, xr.y, xr.z, xr.w};
+        float f[8];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            f[2 * t] = half_bits_to_float(w4[t] & 0xffffu);
+            f[2 * t + 1] = half_bits_to_float(w4[t] >> 16);
+        }
+        float lo[16];
+        nibble_sums(f[0], f[1], f[2], f[3], lo);
+        float* t0 = tab + half * kSliceHalfFloats + slot;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const int h = 2 * kq + hh;
+            const float hv = nibble_sum(f[4], f[5], f[6], f[7], h);
+#pragma unroll
+            for (int l = 0; l < 16; ++l) t0[(16 * h + l) * 64] = lo[l] + hv;
+        }
+    }
+    // LDS writes done, then the barrier; the first job's loads stay in flight
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // Two jobs per iteration, each job's loads issued one job ahead into the
+    // other register set (past the last job the request repeats it), no
+    // branch around the loads, so the compiler keeps both sets in place.
+    for (int k = 0; k < nj; k += 2) {
+        load_job(k + 1, gb);
+        run_job(k, ga);
+        load_job(k + 2, ga);
+        run_job(k + 1, gb);
+    }
+}
+
+// y[n] = sum over slices of part[s][n], in slice order (eight loads in flight
+// per thread, the adds in order).
+__global__ void k_sum_slices(const float* __restrict__ part, int slices, int N,
+                             float* __restrict__ y) {
+    const int n = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (n >= N) return;
+    float s = 0.0f;
+    for (int i0 = 0; i0 < slices; i0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = i0 + u < slices ? part[(size_t)(i0 + u) * N + n] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i0 + u < slices) s = i0 + u == 0 ? v[u] : s + v[u];
+    }
+    y[n] = s;
+}
+
 constexpr int kRowsResidentQ = 4;  // largest q launched two workgroups per CU
 
 // ---------------------------------------------------------------- batch kernel
@@ -1544,6 +1726,59 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
     launch_rows(q, a, plan.workgroups, plan.threads / kRowThreads, s);
+    return launch_status();
+}
+
+// K-slice grid: one workgroup per (slice, row range); the ranges fill one
+// workgroup per CU (256) where there are enough 8-row jobs, at least 16 jobs
+// (one per wave) per range otherwise.
+void kslice_geometry(int N, int K, int* slices, int* ranges, int* jobs) {
+    *slices = K / kSliceCols;
+    *jobs = (N + kSliceJobRows - 1) / kSliceJobRows;
+    int r = 256 / *slices;
+    const int by_jobs = (*jobs + kSliceWaves - 1) / kSliceWaves;
+    if (r > by_jobs) r = by_jobs;
+    *ranges = r < 1 ? 1 : r;
+}
+
+SA_API size_t sa_kslice_workspace_bytes(int N, int K) {
+    if (N < 1 || K < kSliceCols || K % kSliceCols) return 0;
+    return sizeof(float) * (size_t)(K / kSliceCols) * (size_t)N;
+}
+
+SA_API int sa_shiftadd_gemm_kslice(const uint16_t* x, const uint8_t* packed_bits,
+                                   const int8_t* exps, int q, int N, int K, int group, float* y,
+                                   float* workspace, size_t workspace_bytes, void* stream) {
+    const int st = validate_gemm(x, packed_bits, exps, q, N, K, group, 1, y);
+    if (st != SA_OK) return st;
+    if (!workspace) return SA_ERR_NULL;
+    if (group % 128) return SA_ERR_GROUP;
+    if (K % kSliceCols) return SA_ERR_SHAPE;
+    SliceArgs a{};
+    kslice_geometry(N, K, &a.slices, &a.ranges, &a.jobs);
+    if (workspace_bytes < sizeof(float) * (size_t)a.slices * (size_t)N) return SA_ERR_SHAPE;
+    a.x = x;
+    a.packed = packed_bits;
+    a.exps = exps;
+    a.q = q;
+    a.N = N;
+    a.K = K;
+    a.G = group;
+    a.part = workspace;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const dim3 g(a.slices * a.ranges), b(kSliceThreads);
+    switch (q) {
+        case 1: hipLaunchKernelGGL(k_gemm_kslice<1>, g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_gemm_kslice<2>, g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(k_gemm_kslice<3>, g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_gemm_kslice<4>, g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(k_gemm_kslice<5>, g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(k_gemm_kslice<6>, g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(k_gemm_kslice<7>, g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL(k_gemm_kslice<8>, g, b, 0, s, a); break;
+    }
+    hipLaunchKernelGGL(k_sum_slices, dim3((N + 255) / 256), dim3(256), 0, s, workspace, a.slices,
+                       N, y);
     return launch_status();
 }
 

@@ -47,6 +47,8 @@ def _bind(lib):
         "sa_build_lut": ([P, I, I, P, P], I),
         "sa_shiftadd_gemm": ([P, P, P, I, I, I, I, I, P, P], I),
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
+        "sa_kslice_workspace_bytes": ([I, I], ctypes.c_size_t),
+        "sa_shiftadd_gemm_kslice": ([P, P, P, I, I, I, I, P, P, ctypes.c_size_t, P], I),
         "sa_shiftadd_gemm_colwise": ([P, P, P, I, I, I, I, P, P], I),
         "sa_plan_gemm_colwise": ([I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_shiftadd_gemm_blockwise": ([P, P, P, I, I, I, I, I, P, P], I),
@@ -188,6 +190,25 @@ def sa_shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Ten
         _dev(exps, "exps", torch.int8, q * N * (K // group)),
         q, N, K, group, batch,
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm")
+
+
+def sa_kslice_workspace_bytes(N: int, K: int) -> int:
+    return int(lib.sa_kslice_workspace_bytes(N, K))
+
+
+def sa_shiftadd_gemm_kslice(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Tensor,
+                            q: int, N: int, K: int, group: int, y: torch.Tensor,
+                            workspace: torch.Tensor, stream=None) -> None:
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_shiftadd_gemm_kslice")
+    _check(lib.sa_shiftadd_gemm_kslice(
+        _dev(x, "x", torch.float16, K),
+        _dev(packed_bits, "packed_bits", torch.uint8, sa_packed_bytes(q, N, K)),
+        _dev(exps, "exps", torch.int8, q * N * (K // group)),
+        q, N, K, group,
+        _dev(y, "y", torch.float32, N),
+        _dev(workspace, "workspace", torch.float32, workspace.numel()),
+        4 * workspace.numel(), _stream(stream)), "sa_shiftadd_gemm_kslice")
 
 
 def sa_shiftadd_gemm_colwise(x: torch.Tensor, packed_bits: torch.Tensor, col_exps: torch.Tensor,

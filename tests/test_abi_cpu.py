@@ -116,6 +116,25 @@ def test_pack_lut_validation_codes():
     assert L.sa_build_lut(A + 2, 8, 1, A, None) == sa.SA_ERR_ALIGN
 
 
+def test_kslice_validation():
+    L = sa.lib
+    E = sa
+    assert sa.sa_kslice_workspace_bytes(100, 2048) == 4 * 2 * 100
+    assert sa.sa_kslice_workspace_bytes(100, 1536) == 0
+    assert sa.sa_kslice_workspace_bytes(0, 2048) == 0
+    ws = 4 * 2 * 100
+    f = L.sa_shiftadd_gemm_kslice
+    assert f(A, A, A, 3, 100, 2048, 128, A, None, ws, None) == E.SA_ERR_NULL
+    assert f(A, A, None, 3, 100, 2048, 128, A, A, ws, None) == E.SA_ERR_NULL
+    assert f(A, A, A, 9, 100, 2048, 128, A, A, ws, None) == E.SA_ERR_Q
+    assert f(A, A, A, 3, 100, 1536, 128, A, A, ws, None) == E.SA_ERR_SHAPE
+    assert f(A, A, A, 3, 100, 2048, 64, A, A, ws, None) == E.SA_ERR_GROUP
+    assert f(A, A, A, 3, 100, 2048, 100, A, A, ws, None) == E.SA_ERR_GROUP
+    assert f(A, A, A, 3, 100, 2048, 128, A, A, ws - 4, None) == E.SA_ERR_SHAPE
+    assert f(A + 2, A, A, 3, 100, 2048, 128, A, A, ws, None) == E.SA_ERR_ALIGN
+    assert f(A, A, A, 3, 100, 2048, 128, A + 4, A, ws, None) == E.SA_ERR_ALIGN
+
+
 def test_plans():
     p = sa.sa_plan_gemm(3, 4096, 4096, 128, 1)
     assert p["path"] == 1 and p["rows_per_wg"] == 16 and p["workgroups"] == 256

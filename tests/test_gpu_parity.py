@@ -174,6 +174,66 @@ def test_gemm_small(q, N, K, G, B):
     check(gemm(c), y_ref, a_ref, c["name"])
 
 
+# whole-table K-slice layer: 1 to 8 slices; N from 5 rows (one partial 8-row
+# job, waves without jobs) to 28672; ragged last job and last 64-row tile;
+# groups of 128, 256 and 1024 columns; 1, 2, 3, 4 and 8 planes
+KSLICE = [(3, 24576, 2048, 128), (1, 1000, 1024, 128), (4, 28672, 2048, 256),
+          (2, 4100, 8192, 1024), (8, 300, 3072, 128), (3, 8, 1024, 128), (3, 5, 1024, 128)]
+
+
+def gemm_kslice(case, packed=None, ws=None):
+    q, N, K, G = case["q"], case["N"], case["K"], case["G"]
+    if packed is None:
+        packed = pack(case["signs"])
+    if ws is None:
+        ws = torch.full((sa.sa_kslice_workspace_bytes(N, K) // 4,), float("nan"),
+                        dtype=torch.float32, device="cuda")
+    y = torch.full((N,), float("nan"), dtype=torch.float32, device="cuda")
+    sa.sa_shiftadd_gemm_kslice(dev(case["x"]), packed, dev(case["exps"]), q, N, K, G, y, ws)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()[None, :]
+
+
+@pytest.mark.parametrize("q,N,K,G", KSLICE)
+def test_gemm_kslice(q, N, K, G):
+    say(f"gemm kslice q={q} N={N} K={K} G={G}")
+    c = workloads.random_case(q, N, K, G, 1, seed=3, exp_range=(-10, -2), outlier_fraction=0.01)
+    y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], G)
+    packed = pack(c["signs"])
+    y = gemm_kslice(c, packed=packed)
+    check(y, y_ref, a_ref, c["name"])
+    # deterministic, and an exponent shift scales the output exactly
+    assert np.array_equal(gemm_kslice(c, packed=packed), y)
+    c2 = dict(c, exps=(c["exps"] + np.int8(3)).astype(np.int8))
+    assert np.array_equal(gemm_kslice(c2, packed=packed), np.ldexp(y, 3).astype(np.float32))
+
+
+def test_gemm_kslice_workspace_reuse():
+    """One workspace for two layers in a row, the second smaller."""
+    ws = torch.zeros(sa.sa_kslice_workspace_bytes(3000, 4096) // 4, dtype=torch.float32,
+                     device="cuda")
+    for q, N, K in ((3, 3000, 4096), (2, 777, 2048)):
+        say(f"kslice workspace reuse q={q} N={N} K={K}")
+        c = workloads.random_case(q, N, K, 128, 1, seed=4, exp_range=(-10, -2))
+        y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], 128)
+        check(gemm_kslice(c, ws=ws), y_ref, a_ref, c["name"])
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_gemm_kslice_70b_full_size(layer):
+    """The two LLaMA-2-70B MLP shapes at full size, sampled rows (first and last
+    64-row tiles and 512 seeded rows) against the oracle."""
+    d = workloads.layer_inputs("llama2_70b_mlp", layer, 1)
+    q, N, K, G = d["q"], d["N"], d["K"], d["G"]
+    say(f"kslice full size {d['name']} q={q} N={N} K={K}")
+    y = gemm_kslice(d)
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N),
+                                     rng.choice(N, 512, replace=False)]))
+    y_ref, a_ref = oracle.shiftadd_gemm(d["x"], d["signs"], d["exps"], G, rows=rows)
+    check(y[:, rows], y_ref, a_ref, f"{d['name']} (sampled rows)")
+
+
 @pytest.mark.parametrize("B", [2, 5, 8])
 def test_batch_large_activations(B):
     """Activations near the top of the fp16 range in some blocks of some batch
