@@ -648,7 +648,8 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                     a.y[(int64_t)j.b * a.N + n] = s;
                 }
             }
-            __syncthreads();  // red is rewritten by the next batch row
+            // red is rewritten by the next batch row
+            if (j.b + 1 < a.B) __syncthreads();
         }
     };
 
