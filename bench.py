@@ -291,31 +291,54 @@ def bench_layer_set(args) -> int:
     batches = list(w.batches)
     steps = args.steps if args.steps is not None else 200
     warmup = args.warmup if args.warmup is not None else 20
+    # Launch groups: one projection each, or with --fuse the projections of a
+    # decoder layer that read the same input (q, k, v; up, gate) and have the
+    # same bit width concatenated along N into one launch (their rows are
+    # independent, so the layer is the same computation; the group's first
+    # projection's activations serve as the shared input).
+    shared = (("q_proj", "k_proj", "v_proj"), ("up_proj", "gate_proj"))
+    groups, used = [], set()
+    for li, L in enumerate(w.layers):
+        if li in used:
+            continue
+        grp = [li]
+        if args.fuse:
+            for s in shared:
+                if L.name in s:
+                    grp += [lj for lj in range(li + 1, len(w.layers)) if lj not in used
+                            and w.layers[lj].name in s and w.layers[lj].q == L.q]
+        used.update(grp)
+        groups.append(grp)
     t0 = time.perf_counter()
     layers = []
     total_bytes = {B: 0 for B in batches}
     for d in range(w.depth):
-        for li, L in enumerate(w.layers):
-            c = workloads.layer_coins_batches(w.key, li, batches, copy=d)
-            coins = torch.from_numpy(c["coins"]).cuda()
+        for grp in groups:
+            cs = [workloads.layer_coins_batches(w.key, li, batches, copy=d) for li in grp]
+            q, K = w.layers[grp[0]].q, w.layers[grp[0]].K
+            N = sum(w.layers[li].N for li in grp)
+            coins = torch.from_numpy(np.concatenate([c["coins"] for c in cs], axis=1)).cuda()
             shifts = torch.arange(8, device="cuda", dtype=torch.uint8)
             bits = (coins.unsqueeze(-1) >> shifts) & 1            # little-endian bits
-            signs = (bits.to(torch.int8) * 2 - 1).reshape(L.q, L.N, L.K)
+            signs = (bits.to(torch.int8) * 2 - 1).reshape(q, N, K)
             packed = sa.pack_weights(signs)
             del coins, bits, signs
-            xs = {B: torch.from_numpy(c["x"][B]).cuda() for B in batches}
-            ys = {B: torch.empty((B, L.N), dtype=torch.float32, device="cuda") for B in batches}
-            layers.append((L, packed, torch.from_numpy(c["exps"]).cuda(), xs, ys))
+            exps = torch.from_numpy(np.concatenate([c["exps"] for c in cs], axis=1)).cuda()
+            xs = {B: torch.from_numpy(cs[0]["x"][B]).cuda() for B in batches}
+            ys = {B: torch.empty((B, N), dtype=torch.float32, device="cuda") for B in batches}
+            layers.append(((q, N, K), packed, exps, xs, ys))
             for B in batches:
-                total_bytes[B] += algorithmic_bytes(L.q, L.N, L.K, w.group, B)
+                total_bytes[B] += algorithmic_bytes(q, N, K, w.group, B)
     torch.cuda.synchronize()
-    log(f"layer set: {len(layers)} layers generated and packed in {time.perf_counter() - t0:.1f} s")
+    log(f"layer set: {len(layers)} launches per step ({len(groups)} per decoder layer: "
+        f"{[[w.layers[li].name for li in g] for g in groups]}), generated and packed in "
+        f"{time.perf_counter() - t0:.1f} s")
     stream = torch.cuda.Stream()
     res_b = {}
     for B in batches:
         def step():
-            for (L, packed, exps, xs, ys) in layers:
-                sa.sa_shiftadd_gemm(xs[B], packed, exps, L.q, L.N, L.K, w.group, B, ys[B])
+            for ((q, N, K), packed, exps, xs, ys) in layers:
+                sa.sa_shiftadd_gemm(xs[B], packed, exps, q, N, K, w.group, B, ys[B])
 
         with torch.cuda.stream(stream):
             step()
@@ -339,7 +362,8 @@ def bench_layer_set(args) -> int:
         res_b[str(B)] = {"us_per_step": round(us, 2), "tokens_per_s": round(B * 1e6 / us, 1),
                          "GB_per_s": round(gbs, 1), "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
                          "bytes_per_step": total_bytes[B]}
-        log(f"B={B}: {us:.1f} us per 224 layers, {B * 1e6 / us:.1f} tokens/s, {gbs:.1f} GB/s")
+        log(f"B={B}: {us:.1f} us per {len(layers)} launches (224 projections), "
+            f"{B * 1e6 / us:.1f} tokens/s, {gbs:.1f} GB/s")
         del g
     B0 = args.batch or 1
     r0 = res_b[str(B0)]
@@ -359,7 +383,9 @@ def bench_layer_set(args) -> int:
                 "N(0,1) fp16 activations with 1% outlier channels x20); linear layers only",
         "config": {"workload": w.key, "batch": B0, "layers": [f"{L.name} {L.N}x{L.K} q={L.q}"
                                                               for L in w.layers],
-                   "depth": w.depth, "group": w.group, "launch": "hip graph replay"},
+                   "depth": w.depth, "group": w.group, "launch": "hip graph replay",
+                   "launches_per_step": len(layers),
+                   "fused": [[w.layers[li].name for li in g] for g in groups if len(g) > 1]},
         "per_batch": res_b,
         "roofline": {"bound": "hbm", "achieved": r0["GB_per_s"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(r0["GB_per_s"] / HBM_PEAK_GBS, 4),
@@ -602,6 +628,9 @@ def main() -> int:
     ap.add_argument("--terms", type=int, default=0,
                     help="the layer with additive power-of-two factors of this many terms "
                          "(sa_shiftadd_gemm_terms) on the workload layer's shape")
+    ap.add_argument("--fuse", action="store_true",
+                    help="--layer-set: one launch for the projections of a decoder layer "
+                         "that share their input and bit width")
     ap.add_argument("--layer-set", action="store_true",
                     help="time the LLaMA-2-7B decoder layer set (7 projections x 32 layers) at "
                          "batch 1, 4, 8, 16; tokens/s at --batch (default 1)")

@@ -147,6 +147,9 @@ SMALL = [
     (4, 1000, 8320, 128, 1), (3, 4096, 12288, 256, 1), (1, 16, 8192, 8192, 1),
     # ... with two row groups per workgroup (449..512 groups, several pieces)
     (3, 8000, 8320, 128, 1), (2, 8192, 8192, 256, 1),
+    # decoder projections sharing an input run as one launch: q+k at q=2
+    # (8192x4096), up+gate at q=3 (22016x4096)
+    (2, 8192, 4096, 128, 1), (3, 22016, 4096, 128, 1),
     # batch kernel (group % 128 == 0, batch >= 2), 16- and 32-row workgroups
     (2, 300, 384, 128, 2), (3, 257, 1280, 256, 3), (4, 130, 768, 768, 5),
     (2, 1000, 4096, 128, 16), (3, 63, 2048, 128, 4), (2, 129, 1152, 384, 7),
