@@ -301,15 +301,26 @@ __device__ inline void load_job_exps(const RowsArgs& a, int n, int J, int NG, in
         j.e[i] = reinterpret_cast<const uint8_t*>(a.exps + (size_t)i * a.N * NG)[off];
 }
 
-template <int Q>
+// PLANE_ORDER: a workgroup barrier between the planes' requests, so that a
+// CU asks for plane i of every wave before plane i + 1 of any (a CU's loads
+// return in request order); only where every wave of the workgroup runs it.
+template <int Q, bool PLANE_ORDER = false>
 __device__ inline void load_job_keys(const RowsArgs& a, int n, int J, int C, int plane0,
                                      JobRegs<Q>& j) {
     const int T = n >> 6;
     const int R = imin(kTileRows, a.N - kTileRows * T);
     const uint32_t off = (uint32_t)(kTileRows * T * C + 16 * (n & 63) + kBlockChunks * J * R);
 #pragma unroll
-    for (int i = 0; i < Q; ++i)
+    for (int i = 0; i < Q; ++i) {
         j.w[i] = *reinterpret_cast<const uint4*>(a.packed + (size_t)(plane0 + i) * a.N * C + off);
+        if constexpr (PLANE_ORDER) {
+            if (i + 1 < Q) {
+                __builtin_amdgcn_sched_barrier(0);
+                asm volatile("s_barrier" ::: "memory");  // no wait on the loads in flight
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
 }
 
 // Additive: the T exponents and term signs of the lane's group in every plane,
@@ -672,7 +683,10 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
             load_job_terms<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
         else
             load_job_exps<Q>(a, row_of(j), block_of(j), NG, bpg, regs);
-        load_job_keys<Q>(a, row_of(j), block_of(j), C, 0, regs);
+        // 8 waves (H = 1): plane-ordered requests, so every wave's first
+        // plane arrives before any wave's second and all waves query while
+        // the later planes stream in
+        load_job_keys<Q, H == 1>(a, row_of(j), block_of(j), C, 0, regs);
         __builtin_amdgcn_sched_barrier(0);
         build(regs.xr, regs.xe);
         __builtin_amdgcn_sched_barrier(0);
