@@ -147,6 +147,10 @@ SMALL = [
     (4, 1000, 8320, 128, 1), (3, 4096, 12288, 256, 1), (1, 16, 8192, 8192, 1),
     # ... with two row groups per workgroup (449..512 groups, several pieces)
     (3, 8000, 8320, 128, 1), (2, 8192, 8192, 256, 1),
+    # row kernel, one piece and at most 256 row groups (one job per workgroup):
+    # ragged last group, K below 4096 with idle blocks, groups of 256 to 1024
+    (4, 4090, 3840, 256, 1), (1, 200, 1152, 384, 1), (2, 4096, 4096, 128, 1),
+    (3, 31, 2048, 1024, 1),
     # decoder projections sharing an input run as one launch: q+k at q=2
     # (8192x4096), up+gate at q=3 (22016x4096)
     (2, 8192, 4096, 128, 1), (3, 22016, 4096, 128, 1),
