@@ -137,10 +137,11 @@ SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const
  * row) to `workspace`; a second kernel adds each row's partials in slice
  * order into y.  Arguments as for sa_shiftadd_gemm with batch = 1, and:
  *   K % 1024 == 0 and group % 128 == 0 (else SA_ERR_SHAPE, SA_ERR_GROUP);
- *   workspace        (device) fp32, at least sa_kslice_workspace_bytes(N, K)
- *                    bytes = 4 * (K / 1024) * N (else SA_ERR_SHAPE; NULL:
- *                    SA_ERR_NULL); owned by the caller, overwritten; calls
- *                    that share a workspace must not overlap.
+ *   workspace        (device) fp32, 4-byte aligned (else SA_ERR_ALIGN), at
+ *                    least sa_kslice_workspace_bytes(N, K) bytes = 4 * (K /
+ *                    1024) * N (else SA_ERR_SHAPE; NULL: SA_ERR_NULL); owned
+ *                    by the caller, overwritten; calls that share a workspace
+ *                    must not overlap.
  * Deterministic; y is bit-identical across calls but not to sa_shiftadd_gemm
  * (a different fp32 summation order).  Allocates nothing; may be captured in
  * a HIP graph. */

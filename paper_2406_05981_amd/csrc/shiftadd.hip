@@ -1767,6 +1767,7 @@ SA_API int sa_shiftadd_gemm_kslice(const uint16_t* x, const uint8_t* packed_bits
     const int st = validate_gemm(x, packed_bits, exps, q, N, K, group, 1, y);
     if (st != SA_OK) return st;
     if (!workspace) return SA_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 3) return SA_ERR_ALIGN;
     if (group % 128) return SA_ERR_GROUP;
     if (K % kSliceCols) return SA_ERR_SHAPE;
     SliceArgs a{};

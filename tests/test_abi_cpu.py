@@ -133,6 +133,7 @@ def test_kslice_validation():
     assert f(A, A, A, 3, 100, 2048, 128, A, A, ws - 4, None) == E.SA_ERR_SHAPE
     assert f(A + 2, A, A, 3, 100, 2048, 128, A, A, ws, None) == E.SA_ERR_ALIGN
     assert f(A, A, A, 3, 100, 2048, 128, A + 4, A, ws, None) == E.SA_ERR_ALIGN
+    assert f(A, A, A, 3, 100, 2048, 128, A, A + 2, ws, None) == E.SA_ERR_ALIGN
 
 
 def test_plans():
