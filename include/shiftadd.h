@@ -130,6 +130,17 @@ SA_API int sa_build_lut(const uint16_t *x, int K, int batch, float *lut, void *s
 SA_API int sa_shiftadd_gemm(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
                             int q, int N, int K, int group, int batch, float *y, void *stream);
 
+/* The same layer with the output activations in binary16 (Sec. 4.1): y[b][n]
+ * is the fp32 result of sa_shiftadd_gemm rounded to the nearest binary16
+ * (ties to even; beyond the binary16 range +-inf), bit-identical to
+ * converting that fp32 result.  Arguments, launch geometry and errors as for
+ * sa_shiftadd_gemm, with
+ *   y  (device) IEEE binary16 bit patterns [batch][N], 16-byte aligned,
+ *      fully overwritten. */
+SA_API int sa_shiftadd_gemm_f16(const uint16_t *x, const uint8_t *packed_bits, const int8_t *exps,
+                                int q, int N, int K, int group, int batch, uint16_t *y,
+                                void *stream);
+
 /* The same layer at batch 1 with the whole 256-entry table of every chunk
  * (Sec. 4.1), one LDS read and one add per key.  K is cut into 1024-column
  * slices; a workgroup builds the 128 chunk tables of one slice once and

@@ -14,7 +14,7 @@ __all__ = [
     "sa_quantize_bcq_terms", "quantize_bcq_terms", "sa_gram_f16", "sa_inverse_cholesky_diag",
     "sa_importance_criterion", "sa_fit_per_bit", "sa_allocate_bits", "bit_criterion",
     "pack_weights", "shiftadd_gemm", "SaError", "sa_shiftadd_gemm_kslice",
-    "sa_kslice_workspace_bytes",
+    "sa_kslice_workspace_bytes", "sa_shiftadd_gemm_f16",
 ]
 
 

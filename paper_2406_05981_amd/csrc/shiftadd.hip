@@ -39,6 +39,15 @@ __host__ __device__ inline int64_t layout_offset(int i, int n, int c, int N, int
            (int64_t)r * U + p;
 }
 
+// One output: fp32, or IEEE binary16 rounded to nearest even when `half` (the
+// fp16 output activations of Sec. 4.1; y then holds binary16 bit patterns).
+__device__ inline void store_out(float* y, int64_t i, float v, int half) {
+    if (half)
+        reinterpret_cast<uint16_t*>(y)[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
+    else
+        y[i] = v;
+}
+
 __device__ inline float half_bits_to_float(uint32_t h) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
 }
@@ -142,7 +151,8 @@ __global__ void k_build_lut(const uint16_t* __restrict__ x, int K, int B, float*
 // into its total when a group ends.
 __global__ __launch_bounds__(kThreads) void k_gemm_generic(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ packed,
-    const int8_t* __restrict__ exps, int q, int N, int K, int G, float* __restrict__ y) {
+    const int8_t* __restrict__ exps, int q, int N, int K, int G, float* __restrict__ y,
+    int out_half) {
     __shared__ float lut[kBlockChunks][256];
     __shared__ float part[SA_MAX_Q][kThreads];
     const int C = K >> 3, NG = K / G, b = blockIdx.y;
@@ -183,7 +193,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_generic(
         }
         __syncthreads();
     }
-    if (active) y[(int64_t)b * N + n] = total;
+    if (active) store_out(y, (int64_t)b * N + n, total, out_half);
 }
 
 // ---------------------------------------------------------------- row kernel
@@ -504,7 +514,8 @@ __device__ inline float job_sum(JobRegs<Q>& j, uint32_t rgn_lo, uint32_t rgn_hi,
 // H = 2 (layers of several pieces with at most one workgroup per CU): 16
 // waves, the second 8 taking the odd pieces with their own 64 KB of tables, so
 // two pieces are in flight per CU; the 16 waves' row sums meet at the end.
-template <int Q, int U, int MODE, int H = 1>
+// OUT16: y holds binary16 outputs (row-wise layer only).
+template <int Q, int U, int MODE, int H = 1, bool OUT16 = false>
 __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                                                float (*red)[kGroupRows * kMaxRG]) {
     constexpr bool COL = MODE == kColWise;
@@ -656,7 +667,7 @@ __device__ __forceinline__ void gemm_rows_body(const RowsArgs& a, float* lut,
                     float s = red[0][t];
 #pragma unroll
                     for (int w = 1; w < kRowWaves * H; ++w) s += red[w][t];
-                    a.y[(int64_t)j.b * a.N + n] = s;
+                    store_out(a.y, (int64_t)j.b * a.N + n, s, OUT16);
                 }
             }
             // red is rewritten by the next batch row
@@ -732,19 +743,19 @@ constexpr int rows_jobs_per_iter() { return 1; }
 
 // Up to 4 planes: two 8-wave workgroups per CU (4 waves per SIMD, <= 128
 // VGPRs).  More planes need more registers: one workgroup per CU.
-template <int Q, int H = 1>
+template <int Q, int H = 1, bool OUT16 = false>
 __global__ __launch_bounds__(kRowThreads * H) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_rows(RowsArgs a) {
     __shared__ float lut[H * 16 * kRegionFloats];  // 64 KB per half
     __shared__ float red[kRowWaves * H][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise, H>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise, H, OUT16>(a, lut, red);
 }
 
-template <int Q>
+template <int Q, bool OUT16 = false>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_rows_wide(RowsArgs a) {
     __shared__ float lut[16 * kRegionFloats];  // 64 KB
     __shared__ float red[kRowWaves][kGroupRows * kMaxRG];
-    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise>(a, lut, red);
+    gemm_rows_body<Q, rows_jobs_per_iter<Q>(), kRowWise, 1, OUT16>(a, lut, red);
 }
 
 // Column-wise factors: one plane per job, registers of a one-plane job.
@@ -1072,7 +1083,8 @@ __device__ inline void pin_batch_plane(BatchJob<Q, KW>& j, int i) {
 // scattered loads per piece and plane (these touch one cache line per lane
 // and were a third of the additive kernel's time on large layers; the
 // row-wise kernel's one byte per piece measured no gain from it).
-template <int Q, int KW, int MODE, bool UNI = false, bool PRE = false>
+// OUT16: y holds binary16 outputs (row-wise layer only).
+template <int Q, int KW, int MODE, bool UNI = false, bool PRE = false, bool OUT16 = false>
 __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, float* red) {
     constexpr int DS = 4 / KW;  // lanes sharing one row, KW key words each
     constexpr bool ADD = MODE == kAdditive;
@@ -1353,28 +1365,29 @@ __device__ __forceinline__ void gemm_batch_body(const BatchArgs& a, float* lut, 
 #pragma unroll
                 for (int d = 0; d < DS; ++d)
                     s += red[(w * kBatchRows + row * DS + d) * kQuad + u];
-            a.y[(int64_t)b * a.N + nn] = s;
+            store_out(a.y, (int64_t)b * a.N + nn, s, OUT16);
         }
     }
 }
 
 // UNI (block-wise only): every workgroup's rows lie in one block of rows
 // (row_block is a multiple of the 16*KW rows of a workgroup).
-template <int Q, int KW, int MODE = kRowWise, bool UNI = false, bool PRE = false>
+template <int Q, int KW, int MODE = kRowWise, bool UNI = false, bool PRE = false,
+          bool OUT16 = false>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void k_gemm_batch(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];  // 64 KB
     __shared__ float4 red[kRowWaves * kBatchRows];            // 8 KB
-    gemm_batch_body<Q, KW, MODE, UNI, PRE>(a, reinterpret_cast<float*>(lut),
-                                           reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE, UNI, PRE, OUT16>(a, reinterpret_cast<float*>(lut),
+                                                  reinterpret_cast<float*>(red));
 }
 
-template <int Q, int KW, int MODE = kRowWise, bool UNI = false>
+template <int Q, int KW, int MODE = kRowWise, bool UNI = false, bool OUT16 = false>
 __global__ __launch_bounds__(kRowThreads) void k_gemm_batch_wide(BatchArgs a) {
     __shared__ float4 lut[kRowWaves * kWaveTableFloats / 4];
     __shared__ float4 red[kRowWaves * kBatchRows];
-    gemm_batch_body<Q, KW, MODE, UNI>(a, reinterpret_cast<float*>(lut),
-                                      reinterpret_cast<float*>(red));
+    gemm_batch_body<Q, KW, MODE, UNI, false, OUT16>(a, reinterpret_cast<float*>(lut),
+                                                    reinterpret_cast<float*>(red));
 }
 
 // ---------------------------------------------------------------- read probe
@@ -1564,49 +1577,50 @@ int grid_for(int64_t items) {
     return (int)g;
 }
 
+template <bool OUT16 = false>
 void launch_rows(int q, const RowsArgs& a, int workgroups, int split, hipStream_t s) {
     const dim3 g(workgroups), b(kRowThreads * split);
     if (split == 2) {
         switch (q) {
-            case 1: hipLaunchKernelGGL((k_gemm_rows<1, 2>), g, b, 0, s, a); break;
-            case 2: hipLaunchKernelGGL((k_gemm_rows<2, 2>), g, b, 0, s, a); break;
-            case 3: hipLaunchKernelGGL((k_gemm_rows<3, 2>), g, b, 0, s, a); break;
-            default: hipLaunchKernelGGL((k_gemm_rows<4, 2>), g, b, 0, s, a); break;
+            case 1: hipLaunchKernelGGL((k_gemm_rows<1, 2, OUT16>), g, b, 0, s, a); break;
+            case 2: hipLaunchKernelGGL((k_gemm_rows<2, 2, OUT16>), g, b, 0, s, a); break;
+            case 3: hipLaunchKernelGGL((k_gemm_rows<3, 2, OUT16>), g, b, 0, s, a); break;
+            default: hipLaunchKernelGGL((k_gemm_rows<4, 2, OUT16>), g, b, 0, s, a); break;
         }
         return;
     }
     switch (q) {
-        case 1: hipLaunchKernelGGL(k_gemm_rows<1>, g, b, 0, s, a); break;
-        case 2: hipLaunchKernelGGL(k_gemm_rows<2>, g, b, 0, s, a); break;
-        case 3: hipLaunchKernelGGL(k_gemm_rows<3>, g, b, 0, s, a); break;
-        case 4: hipLaunchKernelGGL(k_gemm_rows<4>, g, b, 0, s, a); break;
-        case 5: hipLaunchKernelGGL(k_gemm_rows_wide<5>, g, b, 0, s, a); break;
-        case 6: hipLaunchKernelGGL(k_gemm_rows_wide<6>, g, b, 0, s, a); break;
-        case 7: hipLaunchKernelGGL(k_gemm_rows_wide<7>, g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL(k_gemm_rows_wide<8>, g, b, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_gemm_rows<1, 1, OUT16>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_rows<2, 1, OUT16>), g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_gemm_rows<3, 1, OUT16>), g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_gemm_rows<4, 1, OUT16>), g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((k_gemm_rows_wide<5, OUT16>), g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((k_gemm_rows_wide<6, OUT16>), g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL((k_gemm_rows_wide<7, OUT16>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_rows_wide<8, OUT16>), g, b, 0, s, a); break;
     }
 }
 
-template <int KW, int MODE, bool UNI>
+template <int KW, int MODE, bool UNI, bool OUT16 = false>
 void launch_batch_kw(int q, const BatchArgs& a, int workgroups, hipStream_t s) {
     const dim3 g(workgroups), b(kRowThreads);
     switch (q) {
-        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW, MODE, UNI>), g, b, 0, s, a); break;
-        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW, MODE, UNI>), g, b, 0, s, a); break;
-        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW, MODE, UNI>), g, b, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_gemm_batch<1, KW, MODE, UNI, false, OUT16>), g, b, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_gemm_batch<2, KW, MODE, UNI, false, OUT16>), g, b, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_gemm_batch<3, KW, MODE, UNI, false, OUT16>), g, b, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_gemm_batch<4, KW, MODE, UNI, false, OUT16>), g, b, 0, s, a); break;
+        case 5: hipLaunchKernelGGL((k_gemm_batch_wide<5, KW, MODE, UNI, OUT16>), g, b, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((k_gemm_batch_wide<6, KW, MODE, UNI, OUT16>), g, b, 0, s, a); break;
+        case 7: hipLaunchKernelGGL((k_gemm_batch_wide<7, KW, MODE, UNI, OUT16>), g, b, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_gemm_batch_wide<8, KW, MODE, UNI, OUT16>), g, b, 0, s, a); break;
     }
 }
 
-template <int MODE = kRowWise, bool UNI = false>
+template <int MODE = kRowWise, bool UNI = false, bool OUT16 = false>
 void launch_batch(int q, int kw, const BatchArgs& a, int workgroups, hipStream_t s) {
-    if (kw == 4) launch_batch_kw<4, MODE, UNI>(q, a, workgroups, s);
-    else if (kw == 2) launch_batch_kw<2, MODE, UNI>(q, a, workgroups, s);
-    else launch_batch_kw<1, MODE, UNI>(q, a, workgroups, s);
+    if (kw == 4) launch_batch_kw<4, MODE, UNI, OUT16>(q, a, workgroups, s);
+    else if (kw == 2) launch_batch_kw<2, MODE, UNI, OUT16>(q, a, workgroups, s);
+    else launch_batch_kw<1, MODE, UNI, OUT16>(q, a, workgroups, s);
 }
 
 // Preloaded exponents and term signs (additive batch kernel, up to 3 planes
@@ -1699,8 +1713,9 @@ SA_API int sa_plan_gemm(int q, int N, int K, int group, int batch, sa_plan* plan
     return SA_OK;
 }
 
-SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const int8_t* exps,
-                            int q, int N, int K, int group, int batch, float* y, void* stream) {
+// The layer with fp32 (out_half = 0) or binary16 (out_half = 1) outputs.
+int shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const int8_t* exps, int q, int N,
+                  int K, int group, int batch, float* y, int out_half, void* stream) {
     const int st = validate_gemm(x, packed_bits, exps, q, N, K, group, batch, y);
     if (st != SA_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -1709,7 +1724,7 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     if (plan.path == 0) {
         hipLaunchKernelGGL(k_gemm_generic, dim3((N + kThreads - 1) / kThreads, batch),
                            dim3(kThreads), 0, s,
-                           x, packed_bits, exps, q, N, K, group, y);
+                           x, packed_bits, exps, q, N, K, group, y, out_half);
         return launch_status();
     }
     if (plan.path == 2) {
@@ -1726,7 +1741,10 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
         const int kw = plan.rows_per_wg / 16;
         a.n_tiles = (N + plan.rows_per_wg - 1) / plan.rows_per_wg;
         a.n_quads = (batch + kQuad - 1) / kQuad;
-        launch_batch(q, kw, a, plan.workgroups, s);
+        if (out_half)
+            launch_batch<kRowWise, false, true>(q, kw, a, plan.workgroups, s);
+        else
+            launch_batch(q, kw, a, plan.workgroups, s);
         return launch_status();
     }
     RowsArgs a{};
@@ -1740,8 +1758,23 @@ SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const
     a.B = batch;
     a.y = y;
     a.groups = (N + kGroupRows - 1) / kGroupRows;
-    launch_rows(q, a, plan.workgroups, plan.threads / kRowThreads, s);
+    if (out_half)
+        launch_rows<true>(q, a, plan.workgroups, plan.threads / kRowThreads, s);
+    else
+        launch_rows(q, a, plan.workgroups, plan.threads / kRowThreads, s);
     return launch_status();
+}
+
+SA_API int sa_shiftadd_gemm(const uint16_t* x, const uint8_t* packed_bits, const int8_t* exps,
+                            int q, int N, int K, int group, int batch, float* y, void* stream) {
+    return shiftadd_gemm(x, packed_bits, exps, q, N, K, group, batch, y, 0, stream);
+}
+
+SA_API int sa_shiftadd_gemm_f16(const uint16_t* x, const uint8_t* packed_bits, const int8_t* exps,
+                                int q, int N, int K, int group, int batch, uint16_t* y,
+                                void* stream) {
+    return shiftadd_gemm(x, packed_bits, exps, q, N, K, group, batch,
+                         reinterpret_cast<float*>(y), 1, stream);
 }
 
 // K-slice grid: one workgroup per (slice, row range); the ranges fill one

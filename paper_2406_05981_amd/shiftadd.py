@@ -46,6 +46,7 @@ def _bind(lib):
         "sa_unpack_weights": ([P, I, I, I, P, P], I),
         "sa_build_lut": ([P, I, I, P, P], I),
         "sa_shiftadd_gemm": ([P, P, P, I, I, I, I, I, P, P], I),
+        "sa_shiftadd_gemm_f16": ([P, P, P, I, I, I, I, I, P, P], I),
         "sa_plan_gemm": ([I, I, I, I, I, ctypes.POINTER(SaPlan)], I),
         "sa_kslice_workspace_bytes": ([I, I], ctypes.c_size_t),
         "sa_shiftadd_gemm_kslice": ([P, P, P, I, I, I, I, P, P, ctypes.c_size_t, P], I),
@@ -190,6 +191,19 @@ def sa_shiftadd_gemm(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Ten
         _dev(exps, "exps", torch.int8, q * N * (K // group)),
         q, N, K, group, batch,
         _dev(y, "y", torch.float32, batch * N), _stream(stream)), "sa_shiftadd_gemm")
+
+
+def sa_shiftadd_gemm_f16(x: torch.Tensor, packed_bits: torch.Tensor, exps: torch.Tensor, q: int,
+                         N: int, K: int, group: int, batch: int, y: torch.Tensor,
+                         stream=None) -> None:
+    if group <= 0 or K % group:
+        _check(SA_ERR_GROUP, "sa_shiftadd_gemm_f16")
+    _check(lib.sa_shiftadd_gemm_f16(
+        _dev(x, "x", torch.float16, batch * K),
+        _dev(packed_bits, "packed_bits", torch.uint8, sa_packed_bytes(q, N, K)),
+        _dev(exps, "exps", torch.int8, q * N * (K // group)),
+        q, N, K, group, batch,
+        _dev(y, "y", torch.float16, batch * N), _stream(stream)), "sa_shiftadd_gemm_f16")
 
 
 def sa_kslice_workspace_bytes(N: int, K: int) -> int:

@@ -116,6 +116,16 @@ def test_pack_lut_validation_codes():
     assert L.sa_build_lut(A + 2, 8, 1, A, None) == sa.SA_ERR_ALIGN
 
 
+def test_f16_output_validation():
+    L = sa.lib
+    f = L.sa_shiftadd_gemm_f16
+    assert f(A, A, A, 3, 100, 1024, 128, 1, None, None) == sa.SA_ERR_NULL
+    assert f(A, A, A, 9, 100, 1024, 128, 1, A, None) == sa.SA_ERR_Q
+    assert f(A, A, A, 3, 100, 1024, 100, 1, A, None) == sa.SA_ERR_GROUP
+    assert f(A, A, A, 3, 100, 1024, 128, 0, A, None) == sa.SA_ERR_SHAPE
+    assert f(A, A, A, 3, 100, 1024, 128, 1, A + 2, None) == sa.SA_ERR_ALIGN
+
+
 def test_kslice_validation():
     L = sa.lib
     E = sa

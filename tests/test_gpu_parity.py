@@ -241,6 +241,36 @@ def test_gemm_kslice_70b_full_size(layer):
     check(y[:, rows], y_ref, a_ref, f"{d['name']} (sampled rows)")
 
 
+# binary16 outputs: row kernel (one and several pieces), batch kernel, generic
+# kernel; the last case's outputs exceed the binary16 range
+F16_OUT = [(3, 4096, 4096, 128, 1, (-10, -2)), (3, 1000, 8320, 128, 1, (-10, -2)),
+           (2, 300, 384, 128, 5, (-10, -2)), (4, 130, 768, 768, 16, (-10, -2)),
+           (3, 100, 256, 8, 2, (-10, -2)), (3, 257, 1024, 128, 1, (10, 14))]
+
+
+@pytest.mark.parametrize("q,N,K,G,B,er", F16_OUT)
+def test_gemm_f16_output(q, N, K, G, B, er):
+    say(f"gemm f16 output q={q} N={N} K={K} G={G} B={B} exps {er}")
+    c = workloads.random_case(q, N, K, G, B, seed=6, exp_range=er, outlier_fraction=0.01)
+    packed = pack(c["signs"])
+    y32 = gemm(c, packed=packed)
+    y16 = torch.full((B, N), float("nan"), dtype=torch.float16, device="cuda")
+    sa.sa_shiftadd_gemm_f16(dev(c["x"]), packed, dev(c["exps"]), q, N, K, G, B, y16)
+    torch.cuda.synchronize()
+    y16 = y16.cpu().numpy()
+    with np.errstate(over="ignore"):
+        conv = y32.astype(np.float16)  # IEEE round to nearest even
+    # the fp32 layer's result rounded to binary16, bit for bit
+    assert np.array_equal(y16.view(np.uint16), conv.view(np.uint16))
+    y_ref, a_ref = oracle.shiftadd_gemm(c["x"], c["signs"], c["exps"], G)
+    if er[0] > 0:  # beyond the binary16 range: +-inf, within it: finite
+        big, small = np.abs(y_ref) > 7e4, np.abs(y_ref) < 6e4
+        assert big.any() and np.isinf(y16[big]).all() and np.isfinite(y16[small]).all()
+        return
+    err = np.abs(y16.astype(np.float64) - y_ref)
+    assert (err <= TOL * a_ref + 2.0 ** -11 * np.abs(y_ref) + 2.0 ** -24).all(), c["name"]
+
+
 @pytest.mark.parametrize("B", [2, 5, 8])
 def test_batch_large_activations(B):
     """Activations near the top of the fp16 range in some blocks of some batch
