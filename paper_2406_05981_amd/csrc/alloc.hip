@@ -546,17 +546,22 @@ __global__ __launch_bounds__(256) void k_reverse(const float* __restrict__ H, in
 constexpr int kNB = 64;             // panel width
 constexpr int kNBP = kNB + 1;       // LDS row stride (doubles)
 
-// Diagonal block [j, j + 64) factored in place by one wave, Crout order: lane r
-// holds row r of the block in registers (64 doubles); for column c, lane c
-// finishes its diagonal entry and every lane below it its entry of column c,
-// each a dot product with row c, whose entries are broadcast from lane c
-// (readlane).  A non-positive pivot gives NaN, which then runs through every
-// later value.
+// Broadcast of lane C's value of v (two readlanes).
 template <int C>
 __device__ inline double lane_value(double v) {
     const uint64_t u = __builtin_bit_cast(uint64_t, v);
     const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, C);
     const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), C);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Broadcast of lane Q's value of v to the four lanes of each quad (DPP quad_perm).
+template <int Q>
+__device__ inline double quad_value(double v) {
+    constexpr int ctrl = Q | (Q << 2) | (Q << 4) | (Q << 6);
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)u, ctrl, 0xf, 0xf, false);
+    const uint32_t hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), ctrl, 0xf, 0xf, false);
     return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
@@ -568,79 +573,192 @@ __device__ inline void cfor(F&& f) {
     }
 }
 
-// One wave (lane r = row r of the block).
-__device__ __attribute__((always_inline)) inline void chol_crout(double* __restrict__ A, int K, int j, int r) {
+// Lanes of one wave exchanging data through LDS: the wave's LDS accesses
+// complete in program order, so the exchange needs no hardware barrier, only
+// wavefront-scope ordering.  Without it the compiler may move a lane's read of
+// another lane's entry across the write that fills it (per thread it can prove
+// the two addresses differ).
+__device__ inline void lds_exchange() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 1 / sqrt(p): the hardware estimate (v_rsq_f64) refined by two Newton-Raphson
+// steps y <- y + y (1 - p y^2) / 2, within a few ulp; p <= 0 gives NaN.
+__device__ inline double rsqrt_nr(double p) {
+    double y = __builtin_amdgcn_rsq(p);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const double e = fma(-p * y, y, 1.0);
+        y = fma(0.5 * y, e, y);
+    }
+    return y;
+}
+
+// Diagonal block [j, j + 64) factored in place by one wave, right-looking, lane
+// r holding row r of the block in registers (64 doubles).  At step c, with
+// pivot p (lane c's entry c) and rd = 1 / sqrt(p): L[c][c] = p rd, the lanes
+// below scale their entry of column c by rd, publish it in LDS and subtract
+// their multiple of column c from their entries c + 1 .. 63, reading the column
+// back as broadcasts (a single wave needs no barrier: its LDS accesses complete
+// in order).  The next pivot is formed on the side from lane c + 1's own
+// entries, so the LDS round trip stays off the chain of pivots, and each step's
+// reads are issued together before its FMAs.  Entries above the diagonal are
+// never read: the lanes compute them unmasked.  The block passes through LDS
+// (`stage`, 64 x 65 doubles) on the way in and out, so every global access
+// covers a whole row; the lower triangle is stored in place and its transpose
+// in the block's upper triangle (row c there = column c of L), which the panel
+// solve reads contiguously.  A non-positive pivot gives NaN, which then runs
+// through every later value.
+__device__ __attribute__((always_inline)) inline void chol_block(double* __restrict__ A, int K, int j, int r,
+                                                               double* __restrict__ stage) {
     const int nb = min(kNB, K - j);
+    const int cl = min(r, nb - 1);     // this lane's column for the row-wise copies
+    {
+        double v[kNB];
+#pragma unroll
+        for (int rr = 0; rr < kNB; ++rr) v[rr] = A[(int64_t)(j + min(rr, nb - 1)) * K + j + cl];
+#pragma unroll
+        for (int rr = 0; rr < kNB; ++rr) stage[rr * kNBP + r] = v[rr];
+    }
+    lds_exchange();
     double a[kNB];
     cfor<0, kNB>([&](auto c_) {
         constexpr int c = decltype(c_)::value;
-        a[c] = (r < nb && c < nb && c <= r) ? A[(int64_t)(j + r) * K + j + c] : (c == r ? 1.0 : 0.0);
+        const double v = stage[r * kNBP + c];
+        a[c] = (r < nb && c <= r) ? v : (c == r ? 1.0 : 0.0);
+    });
+    lds_exchange();
+    double* col = stage;               // the staged block is dead while the factorization runs
+    double p = lane_value<0>(a[0]);
+    cfor<0, kNB>([&](auto c_) {
+        constexpr int c = decltype(c_)::value;
+        const double rd = rsqrt_nr(p);
+        const double l = a[c] * rd;
+        a[c] = r == c ? p * rd : l;
+        col[r] = l;
+        if constexpr (c + 1 < kNB) p = lane_value<c + 1>(fma(-l, l, a[c + 1]));
+        constexpr int n = kNB - 1 - c;
+        if constexpr (n > 0) {
+            double v[n];
+            cfor<0, n>([&](auto i_) {
+                constexpr int i = decltype(i_)::value;
+                v[i] = col[c + 1 + i];
+            });
+            __builtin_amdgcn_sched_barrier(0);
+            cfor<0, n>([&](auto i_) {
+                constexpr int i = decltype(i_)::value;
+                a[c + 1 + i] = fma(-l, v[i], a[c + 1 + i]);
+            });
+        }
     });
     cfor<0, kNB>([&](auto c_) {
         constexpr int c = decltype(c_)::value;
-        // row c's finished entries 0..c-1, from lane c
-        double rc[c > 0 ? c : 1];
-        cfor<0, c>([&](auto k_) {
-            constexpr int k = decltype(k_)::value;
-            rc[k] = lane_value<c>(a[k]);
-        });
-        double v = a[c];
-        cfor<0, c>([&](auto k_) {
-            constexpr int k = decltype(k_)::value;
-            v = fma(-a[k], rc[k], v);
-        });
-        // lane c: the pivot; lanes below: divide by it
-        const double piv = lane_value<c>(r == c ? sqrt(v) : 0.0);
-        if (r == c) a[c] = piv;
-        else if (r > c) a[c] = v / piv;
+        stage[r * kNBP + c] = a[c];
     });
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        if (r < nb && c < nb && c <= r) A[(int64_t)(j + r) * K + j + c] = a[c];
-    });
+    lds_exchange();
+    // row rr of the block: L[rr][c] for c <= rr, L[c][rr] above the diagonal
+#pragma unroll
+    for (int rr = 0; rr < kNB; ++rr) {
+        const double v = r <= rr ? stage[rr * kNBP + r] : stage[r * kNBP + rr];
+        if (rr < nb && r < nb) A[(int64_t)(j + rr) * K + j + r] = v;
+    }
 }
 
 // The first diagonal block; later ones are factored by the trailing update
 // that finishes them (k_chol_syrk).
 __global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K, int j) {
-    chol_crout(A, K, j, threadIdx.x);
+    __shared__ double stage[kNB * kNBP];
+    chol_block(A, K, j, threadIdx.x, stage);
 }
 
-// Panel below the diagonal block: row r (r >= j + 64) solves x L11^T = a, one
-// row per lane held in registers, L11 in LDS (every lane reads the same entry:
-// a broadcast).
-__global__ __launch_bounds__(64) void k_chol_trsm(double* __restrict__ A, int K, int j) {
-    __shared__ double l11[kNB * kNB];
-    for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
-        const int rr = e / kNB, c = e % kNB;
-        l11[e] = c <= rr ? A[(int64_t)(j + rr) * K + j + c] : 0.0;
+constexpr int kQS = 18;   // LDS stride (doubles) of one (c, q) run of 16 entries of L11
+
+// Panel below the diagonal block: rows r >= j + 64 solve x L11^T = a, 64 rows
+// per workgroup of four waves.  Each row is split over the four lanes of a
+// quad: lane l of wave w takes row 16 w + l / 4 and its columns 4 m + (l mod 4),
+// m = 0 .. 15, in registers.  Right-looking: at step c the lane holding x_c
+// scales it by 1 / L11[c][c], the quad shares it (DPP), and each lane subtracts
+// its multiple of column c of L11 from its own later entries.  Column c of L11
+// is row c of the block's upper triangle (written there by chol_block), held in
+// LDS per quad lane; its entries do not depend on x, so the next step's are read
+// during the current step's FMAs.  Launched only where the panel has rows below,
+// so the diagonal block is whole.
+__global__ __launch_bounds__(256) void k_chol_trsm(double* __restrict__ A, int K, int j) {
+    __shared__ double lt[kNB * 4 * kQS];   // lt[(c * 4 + q) * kQS + m] = L11[4 m + q][c] if 4 m + q > c, else 0
+    __shared__ double rv[kNB];             // 1 / L11[k][k]
+    const int t = threadIdx.x;
+    {
+        double v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int e = t + 256 * i, c = e >> 6, k = e & 63;
+            v[i] = A[(int64_t)(j + c) * K + j + k];
+        }
+        const double dg = A[(int64_t)(j + (t & 63)) * K + j + (t & 63)];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int e = t + 256 * i, c = e >> 6, k = e & 63;
+            lt[(c * 4 + (k & 3)) * kQS + (k >> 2)] = k > c ? v[i] : 0.0;
+        }
+        if (t < kNB) rv[t] = 1.0 / dg;
     }
+    const int w = t >> 6, l = t & 63, q = l & 3;
+    const int row = j + kNB + blockIdx.x * kNB + 16 * w + (l >> 2);
+    const int rowc = min(row, K - 1);
+    double x[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) x[m] = A[(int64_t)rowc * K + j + 4 * m + q];
     __syncthreads();
-    const int row = j + kNB + blockIdx.x * 64 + threadIdx.x;
-    const bool ok = row < K;
-    double x[kNB];
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        x[c] = ok ? A[(int64_t)row * K + j + c] : 0.0;
+    double rq[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) rq[m] = rv[4 * m + q];
+    const double* ltq = lt + q * kQS;
+    double cur[16], nxt[16];
+    cfor<0, 16>([&](auto m_) {
+        constexpr int m = decltype(m_)::value;
+        cur[m] = ltq[m];
     });
     cfor<0, kNB>([&](auto c_) {
         constexpr int c = decltype(c_)::value;
-        double v = x[c];
-        cfor<0, c>([&](auto k_) {
-            constexpr int k = decltype(k_)::value;
-            v = fma(-x[k], l11[c * kNB + k], v);
+        constexpr int m0 = c / 4, q0 = c % 4;
+        if constexpr (c + 1 < kNB) {
+            cfor<(c + 1) / 4, 16>([&](auto m_) {
+                constexpr int m = decltype(m_)::value;
+                nxt[m] = ltq[(c + 1) * 4 * kQS + m];
+            });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const double xc = quad_value<q0>(x[m0] * rq[m0]);
+        cfor<m0, 16>([&](auto m_) {
+            constexpr int m = decltype(m_)::value;
+            x[m] = fma(-xc, cur[m], x[m]);
         });
-        x[c] = v / l11[c * kNB + c];
+        x[m0] = q == q0 ? xc : x[m0];
+        if constexpr (c + 1 < kNB) {
+            cfor<(c + 1) / 4, 16>([&](auto m_) {
+                constexpr int m = decltype(m_)::value;
+                cur[m] = nxt[m];
+            });
+        }
     });
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        if (ok) A[(int64_t)row * K + j + c] = x[c];
-    });
+    if (row < K) {
+#pragma unroll
+        for (int m = 0; m < 16; ++m) A[(int64_t)row * K + j + 4 * m + q] = x[m];
+    }
 }
+
+typedef double double4v __attribute__((ext_vector_type(4)));
 
 // Trailing update of the lower triangle: A[r][s] -= sum_c L[r][c] L[s][c] over
-// the panel's 64 columns, for 64 x 64 tiles (tr >= ts) below the panel.  Each
-// thread owns 4 x 4 entries of the tile.
+// the panel's 64 columns, for 64 x 64 tiles (tr >= ts) below the panel, on the
+// fp64 matrix cores.  Each wave takes a 32 x 32 quarter of the tile (2 x 2
+// blocks of 16 x 16; a diagonal tile's upper quarter is skipped).  The panel
+// rows and the tile's current values are loaded together, every load in flight
+// before the first LDS write.  Operand layout of v_mfma_f64_16x16x4_f64: lane l
+// holds A[l mod 16][l / 16] and B[l / 16][l mod 16]; result register q holds
+// row 4 q + l / 16 of column l mod 16.
 __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K, int j) {
     __shared__ double lr_[kNB * kNBP];
     __shared__ double ls_[kNB * kNBP];
@@ -651,47 +769,76 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
     const int ts = b - tr * (tr + 1) / 2;
     const int base = j + kNB;
     const int r0 = base + tr * kNB, s0 = base + ts * kNB;
-    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
-        const int r = e / kNB, c = e % kNB;
-        lr_[r * kNBP + c] = r0 + r < K ? A[(int64_t)(r0 + r) * K + j + c] : 0.0;
-        ls_[r * kNBP + c] = s0 + r < K ? A[(int64_t)(s0 + r) * K + j + c] : 0.0;
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    const int qr = (w >> 1) * 32, qs = (w & 1) * 32;
+    const int li = l & 15, lk = l >> 4;
+    const bool live = !(tr == ts && qs > qr);
+    double cur[2][2][4];
+    {
+        // rows past the matrix repeat its last row: their products are never stored
+        double vr[16], vs[16];
+        const int c = threadIdx.x & 63, rr = threadIdx.x >> 6;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            vr[i] = A[(int64_t)min(r0 + rr + 4 * i, K - 1) * K + j + c];
+            vs[i] = A[(int64_t)min(s0 + rr + 4 * i, K - 1) * K + j + c];
+        }
+        if (live) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int v = 0; v < 2; ++v)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int r = min(r0 + qr + 16 * u + lk + 4 * q, K - 1);
+                        const int s = min(s0 + qs + 16 * v + li, K - 1);
+                        cur[u][v][q] = A[(int64_t)r * K + s];
+                    }
+        }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            lr_[(rr + 4 * i) * kNBP + c] = vr[i];
+            ls_[(rr + 4 * i) * kNBP + c] = vs[i];
+        }
     }
     __syncthreads();
-    // thread (ty, tx) owns rows ty + 16 u and columns tx + 16 v: the 16 lanes of
-    // a read cover 16 consecutive rows (no bank conflicts with the 65-double
-    // stride) and the update writes 128-byte runs
-    const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
-    double acc[4][4];
+    if (live) {
+        double4v acc[2][2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-    for (int c = 0; c < kNB; ++c) {
-        double a4[4], b4[4];
+            for (int v = 0; v < 2; ++v) acc[u][v] = (double4v){0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            a4[u] = lr_[(ty + 16 * u) * kNBP + c];
-            b4[u] = ls_[(tx + 16 * u) * kNBP + c];
+        for (int c = 0; c < kNB; c += 4) {
+            double av[2], bv[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                av[u] = lr_[(qr + 16 * u + li) * kNBP + c + lk];
+                bv[u] = ls_[(qs + 16 * u + li) * kNBP + c + lk];
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int v = 0; v < 2; ++v)
+                    acc[u][v] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[u], bv[v], acc[u][v], 0, 0, 0);
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[u][v] = fma(a4[u], b4[v], acc[u][v]);
+            for (int v = 0; v < 2; ++v)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int r = r0 + qr + 16 * u + lk + 4 * q, s = s0 + qs + 16 * v + li;
+                    if (r < K && s < K && s <= r) A[(int64_t)r * K + s] = cur[u][v][q] - acc[u][v][q];
+                }
     }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = r0 + ty + 16 * u, s = s0 + tx + 16 * v;
-            if (r < K && s < K && s <= r) A[(int64_t)r * K + s] -= acc[u][v];
-        }
     // Tile (0, 0) is the next panel's diagonal block, final once this tile is
     // written: its first wave factors it while the other tiles are still being
     // updated (one launch per panel fewer, and the factorization off the
     // critical path wherever the update takes longer than it).
     if (b == 0) {
         __syncthreads();
-        if (threadIdx.x < 64) chol_crout(A, K, base, (int)threadIdx.x);
+        if (threadIdx.x < 64) chol_block(A, K, base, (int)threadIdx.x, lr_);
     }
 }
 
@@ -813,7 +960,7 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
         const int below = K - j - kNB;
         if (below > 0) {
             const int rb = (below + kNB - 1) / kNB;
-            hipLaunchKernelGGL(k_chol_trsm, dim3((below + 63) / 64), dim3(64), 0, s, A, K, j);
+            hipLaunchKernelGGL(k_chol_trsm, dim3((below + 63) / 64), dim3(256), 0, s, A, K, j);
             hipLaunchKernelGGL(k_chol_syrk, dim3(rb * (rb + 1) / 2), dim3(256), 0, s, A, K, j);
         }
     }
