@@ -546,6 +546,8 @@ __global__ __launch_bounds__(256) void k_reverse(const float* __restrict__ H, in
 constexpr int kNB = 64;             // panel width
 constexpr int kNBP = kNB + 1;       // LDS row stride (doubles)
 
+typedef double double4v __attribute__((ext_vector_type(4)));
+
 // Broadcast of lane C's value of v (two readlanes).
 template <int C>
 __device__ inline double lane_value(double v) {
@@ -596,81 +598,116 @@ __device__ inline double rsqrt_nr(double p) {
     return y;
 }
 
-// Diagonal block [j, j + 64) factored in place by one wave, right-looking, lane
-// r holding row r of the block in registers (64 doubles).  At step c, with
-// pivot p (lane c's entry c) and rd = 1 / sqrt(p): L[c][c] = p rd, the lanes
-// below scale their entry of column c by rd, publish it in LDS and subtract
-// their multiple of column c from their entries c + 1 .. 63, reading the column
-// back as broadcasts (a single wave needs no barrier: its LDS accesses complete
-// in order).  The next pivot is formed on the side from lane c + 1's own
-// entries, so the LDS round trip stays off the chain of pivots, and each step's
-// reads are issued together before its FMAs.  Entries above the diagonal are
-// never read: the lanes compute them unmasked.  The block passes through LDS
-// (`stage`, 64 x 65 doubles) on the way in and out, so every global access
-// covers a whole row; the lower triangle is stored in place and its transpose
-// in the block's upper triangle (row c there = column c of L), which the panel
-// solve reads contiguously.  A non-positive pivot gives NaN, which then runs
-// through every later value.
-__device__ __attribute__((always_inline)) inline void chol_block(double* __restrict__ A, int K, int j, int r,
-                                                               double* __restrict__ stage) {
+// Diagonal block [j, j + 64) factored in place by a workgroup of four waves
+// (256 threads), blocked: the block sits in LDS (`S`, 64 x 65 doubles, lower
+// triangle; rows and columns past the matrix as identity), and for each
+// 16-column sub-panel
+//  - the first wave factors it right-looking, lane r holding row r's 16
+//    entries: at step c, with pivot p (lane c's entry) and rd = 1 / sqrt(p),
+//    L[c][c] = p rd, the other lanes scale their entry of column c by rd,
+//    publish it in LDS (`col`, 64 doubles) and subtract their multiple of it
+//    from their later entries of the sub-panel, reading the column back as
+//    broadcasts (at most 15 per step); the next pivot is formed on the side
+//    from its own lane's entries, so the LDS round trip stays off the chain
+//    of pivots;
+//  - the four waves subtract its product with itself from the later columns,
+//    16 x 16 blocks of the lower triangle on the fp64 matrix cores.
+// Entries above the diagonal are never read.  Every global access is a whole
+// row: the lower triangle is stored in place and its transpose in the block's
+// upper triangle (row c there = column c of L), which the panel solve reads
+// contiguously.  A non-positive pivot gives NaN, which then runs through every
+// later value.
+__device__ __attribute__((always_inline)) inline void chol_block(double* __restrict__ A, int K, int j,
+                                                               double* __restrict__ S, double* __restrict__ col) {
+    const int t = threadIdx.x, w = t >> 6, r = t & 63;
     const int nb = min(kNB, K - j);
-    const int cl = min(r, nb - 1);     // this lane's column for the row-wise copies
     {
-        double v[kNB];
+        const int cl = min(r, nb - 1);
+        double v[16];
 #pragma unroll
-        for (int rr = 0; rr < kNB; ++rr) v[rr] = A[(int64_t)(j + min(rr, nb - 1)) * K + j + cl];
+        for (int i = 0; i < 16; ++i) v[i] = A[(int64_t)(j + min(w + 4 * i, nb - 1)) * K + j + cl];
 #pragma unroll
-        for (int rr = 0; rr < kNB; ++rr) stage[rr * kNBP + r] = v[rr];
+        for (int i = 0; i < 16; ++i) {
+            const int rr = w + 4 * i;
+            S[rr * kNBP + r] = (rr < nb && r < nb && r <= rr) ? v[i] : (rr == r ? 1.0 : 0.0);
+        }
     }
-    lds_exchange();
-    double a[kNB];
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        const double v = stage[r * kNBP + c];
-        a[c] = (r < nb && c <= r) ? v : (c == r ? 1.0 : 0.0);
-    });
-    lds_exchange();
-    double* col = stage;               // the staged block is dead while the factorization runs
-    double p = lane_value<0>(a[0]);
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        const double rd = rsqrt_nr(p);
-        const double l = a[c] * rd;
-        a[c] = r == c ? p * rd : l;
-        col[r] = l;
-        if constexpr (c + 1 < kNB) p = lane_value<c + 1>(fma(-l, l, a[c + 1]));
-        constexpr int n = kNB - 1 - c;
-        if constexpr (n > 0) {
-            double v[n];
-            cfor<0, n>([&](auto i_) {
-                constexpr int i = decltype(i_)::value;
-                v[i] = col[c + 1 + i];
+    __syncthreads();
+    const int li = r & 15, lk = r >> 4;
+    cfor<0, 4>([&](auto s_) {
+        constexpr int s = decltype(s_)::value;
+        constexpr int c0 = 16 * s;
+        if (w == 0) {
+            double a[16];
+            cfor<0, 16>([&](auto k_) {
+                constexpr int k = decltype(k_)::value;
+                a[k] = S[r * kNBP + c0 + k];
             });
-            __builtin_amdgcn_sched_barrier(0);
-            cfor<0, n>([&](auto i_) {
-                constexpr int i = decltype(i_)::value;
-                a[c + 1 + i] = fma(-l, v[i], a[c + 1 + i]);
+            double p = lane_value<c0>(a[0]);
+            cfor<0, 16>([&](auto cc_) {
+                constexpr int cc = decltype(cc_)::value;
+                constexpr int c = c0 + cc;
+                const double rd = rsqrt_nr(p);
+                const double l = a[cc] * rd;
+                a[cc] = r == c ? p * rd : l;
+                col[r] = l;
+                lds_exchange();
+                if constexpr (cc + 1 < 16) p = lane_value<c + 1>(fma(-l, l, a[cc + 1]));
+                constexpr int n = 15 - cc;
+                if constexpr (n > 0) {
+                    double v[n];
+                    cfor<0, n>([&](auto i_) {
+                        constexpr int i = decltype(i_)::value;
+                        v[i] = col[c + 1 + i];
+                    });
+                    __builtin_amdgcn_sched_barrier(0);
+                    cfor<0, n>([&](auto i_) {
+                        constexpr int i = decltype(i_)::value;
+                        a[cc + 1 + i] = fma(-l, v[i], a[cc + 1 + i]);
+                    });
+                }
+            });
+            cfor<0, 16>([&](auto k_) {
+                constexpr int k = decltype(k_)::value;
+                S[r * kNBP + c0 + k] = a[k];
             });
         }
-    });
-    cfor<0, kNB>([&](auto c_) {
-        constexpr int c = decltype(c_)::value;
-        stage[r * kNBP + c] = a[c];
-    });
-    lds_exchange();
-    // row rr of the block: L[rr][c] for c <= rr, L[c][rr] above the diagonal
+        __syncthreads();
+        if constexpr (s < 3) {
+            // blocks (bi, bj), s < bj <= bi <= 3, numbered row by row over that triangle
+            constexpr int m = 3 - s, nblk = m * (m + 1) / 2;
+            for (int bk = w; bk < nblk; bk += 4) {
+                int bi = 0;
+                while ((bi + 1) * (bi + 2) / 2 <= bk) ++bi;
+                const int bj = bk - bi * (bi + 1) / 2;
+                const int R0 = 16 * (s + 1 + bi), C0 = 16 * (s + 1 + bj);
+                double4v acc = (double4v){0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int rr = 0; rr < kNB; ++rr) {
-        const double v = r <= rr ? stage[rr * kNBP + r] : stage[r * kNBP + rr];
+                for (int kk = 0; kk < 4; ++kk) {
+                    const double av = S[(R0 + li) * kNBP + c0 + 4 * kk + lk];
+                    const double bv = S[(C0 + li) * kNBP + c0 + 4 * kk + lk];
+                    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc, 0, 0, 0);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) S[(R0 + lk + 4 * q) * kNBP + C0 + li] -= acc[q];
+            }
+            __syncthreads();
+        }
+    });
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int rr = w + 4 * i;
+        const double v = r <= rr ? S[rr * kNBP + r] : S[r * kNBP + rr];
         if (rr < nb && r < nb) A[(int64_t)(j + rr) * K + j + r] = v;
     }
 }
 
 // The first diagonal block; later ones are factored by the trailing update
 // that finishes them (k_chol_syrk).
-__global__ __launch_bounds__(64) void k_chol_diag(double* __restrict__ A, int K, int j) {
-    __shared__ double stage[kNB * kNBP];
-    chol_block(A, K, j, threadIdx.x, stage);
+__global__ __launch_bounds__(256) void k_chol_diag(double* __restrict__ A, int K, int j) {
+    __shared__ double S[kNB * kNBP];
+    __shared__ double col[kNB];
+    chol_block(A, K, j, S, col);
 }
 
 constexpr int kQS = 18;   // LDS stride (doubles) of one (c, q) run of 16 entries of L11
@@ -748,8 +785,6 @@ __global__ __launch_bounds__(256) void k_chol_trsm(double* __restrict__ A, int K
         for (int m = 0; m < 16; ++m) A[(int64_t)row * K + j + 4 * m + q] = x[m];
     }
 }
-
-typedef double double4v __attribute__((ext_vector_type(4)));
 
 // Trailing update of the lower triangle: A[r][s] -= sum_c L[r][c] L[s][c] over
 // the panel's 64 columns, for 64 x 64 tiles (tr >= ts) below the panel, on the
@@ -833,12 +868,12 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
                 }
     }
     // Tile (0, 0) is the next panel's diagonal block, final once this tile is
-    // written: its first wave factors it while the other tiles are still being
+    // written: its workgroup factors it while the other tiles are still being
     // updated (one launch per panel fewer, and the factorization off the
     // critical path wherever the update takes longer than it).
     if (b == 0) {
         __syncthreads();
-        if (threadIdx.x < 64) chol_block(A, K, base, (int)threadIdx.x, lr_);
+        chol_block(A, K, base, lr_, ls_);
     }
 }
 
@@ -955,7 +990,7 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
     const int64_t n = (int64_t)K * K;
     const int grid = (int)(((n + 255) / 256) < 8192 ? (n + 255) / 256 : 8192);
     hipLaunchKernelGGL(k_reverse, dim3(grid), dim3(256), 0, s, H, K, lambda, A);
-    hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(64), 0, s, A, K, 0);
+    hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(256), 0, s, A, K, 0);
     for (int j = 0; j < K; j += kNB) {
         const int below = K - j - kNB;
         if (below > 0) {
