@@ -88,7 +88,10 @@ def test_gram_repeatable(K, T):
 
 
 @pytest.mark.parametrize("K,T,damp", [(64, 256, 0.01), (200, 512, 0.01), (384, 256, 0.05),
-                                      (1000, 2048, 0.01), (130, 1024, 0.0)])
+                                      (1000, 2048, 0.01), (130, 1024, 0.0),
+                                      # last diagonal block of 1, 63 and 1 rows; whole panels only
+                                      (65, 256, 0.01), (127, 512, 0.01), (129, 512, 0.01),
+                                      (256, 1024, 0.01)])
 def test_inverse_cholesky_diag(K, T, damp):
     """Including K not a multiple of the 64-column panel, and no damping on a
     full-rank calibration set."""
@@ -100,6 +103,26 @@ def test_inverse_cholesky_diag(K, T, damp):
     ref = alloc.cholesky_diag_of_inverse(alloc.damped(H32.astype(np.float64), damp))
     assert np.all(np.isfinite(d))
     assert np.allclose(d, ref, rtol=1e-9, atol=0)
+
+
+@pytest.mark.parametrize("K,m", [(300, 100), (200, 199), (130, 0)])
+def test_inverse_cholesky_not_positive_definite(K, m):
+    """The documented behaviour for a matrix that is not positive definite:
+    channel m made to fail (its pivot, taken after the later channels in the
+    reversed order, is negative).  d[k] for k > m depends only on the later
+    channels and matches the oracle on that trailing block; d[0..m] are NaN."""
+    say(f"not positive definite K={K} m={m}")
+    x = calib(K, 4 * K, seed=K + m)
+    x64 = x.astype(np.float64)
+    H = x64 @ x64.T
+    H[m, m] = -1000.0 * abs(H[m, m])
+    H32 = H.astype(np.float32)
+    d = gpu_d(torch.from_numpy(H32).cuda(), 0.0)
+    assert np.all(np.isnan(d[:m + 1]))
+    if m + 1 < K:
+        ref = alloc.cholesky_diag_of_inverse(alloc.damped(H32[m + 1:, m + 1:].astype(np.float64), 0.0))
+        assert np.all(np.isfinite(d[m + 1:]))
+        assert np.allclose(d[m + 1:], ref, rtol=1e-9, atol=0)
 
 
 def test_criterion_from_d():
