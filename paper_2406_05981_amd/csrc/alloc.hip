@@ -527,17 +527,47 @@ __global__ __launch_bounds__(256) void k_damping(const float* __restrict__ H, in
     if (threadIdx.x == 0) *lambda = damp * (part[0] / K);
 }
 
-// A = J H J + lambda I in fp64 (lower triangle and diagonal), J the reversal.
+// Lower-triangular tile (ti, tj), ti >= tj, of linear block index b.
+__device__ inline void lower_tile(int b, int& ti, int& tj) {
+    int t = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
+    while ((t + 1) * (t + 2) / 2 <= b) ++t;
+    while (t * (t + 1) / 2 > b) --t;
+    ti = t;
+    tj = b - t * (t + 1) / 2;
+}
+
+// A = J H J + lambda I in fp64 (lower triangle and diagonal), J the reversal:
+// A[i][j] = H[K-1-j][K-1-i] for j <= i, from H's lower triangle.  One 64 x 64
+// tile of A on or below the diagonal per workgroup, passed through LDS so that
+// the reads of H and the writes of A both run along rows.
 __global__ __launch_bounds__(256) void k_reverse(const float* __restrict__ H, int K,
                                                  const double* __restrict__ lambda,
                                                  double* __restrict__ A) {
-    const int64_t n = (int64_t)K * K;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
-        const int i = (int)(e / K), j = (int)(e % K);
-        if (j > i) continue;
-        double v = (double)H[(int64_t)(K - 1 - j) * K + (K - 1 - i)];
-        if (i == j) v += *lambda;
-        A[e] = v;
+    __shared__ float S[64 * 65];
+    int ti, tj;
+    lower_tile((int)blockIdx.x, ti, tj);
+    const int i0 = 64 * ti, j0 = 64 * tj;
+    // source block: rows K - j0 - 64 .. K - j0 - 1, columns K - i0 - 64 .. K - i0 - 1 of H
+    const int a0 = K - j0 - 64, c0 = K - i0 - 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int a = a0 + ty + 4 * k, c = c0 + tx;
+        v[k] = (a >= 0 && c >= 0 && c <= a) ? H[(int64_t)a * K + c] : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) S[(ty + 4 * k) * 65 + tx] = v[k];
+    __syncthreads();
+    const double lam = *lambda;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int r = ty + 4 * k, i = i0 + r, j = j0 + tx;
+        if (i < K && j <= i) {
+            double val = (double)S[(63 - tx) * 65 + (63 - r)];
+            if (i == j) val += lam;
+            A[(int64_t)i * K + j] = val;
+        }
     }
 }
 
@@ -798,10 +828,8 @@ __global__ __launch_bounds__(256) void k_chol_syrk(double* __restrict__ A, int K
     __shared__ double lr_[kNB * kNBP];
     __shared__ double ls_[kNB * kNBP];
     const int b = blockIdx.x;
-    int tr = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
-    while ((tr + 1) * (tr + 2) / 2 <= b) ++tr;
-    while (tr * (tr + 1) / 2 > b) --tr;
-    const int ts = b - tr * (tr + 1) / 2;
+    int tr, ts;
+    lower_tile(b, tr, ts);
     const int base = j + kNB;
     const int r0 = base + tr * kNB, s0 = base + ts * kNB;
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -888,29 +916,50 @@ __global__ __launch_bounds__(256) void k_inverse_diag(const double* __restrict__
 
 constexpr int kStatBlocks = 1024;
 
-// Per-block fp64 sums of IS and IS^2 (grid-strided, fixed order per block).
+// Per-block fp64 sums of IS and IS^2 over rows blockIdx.x, blockIdx.x +
+// gridDim.x, ...: each thread takes columns t, t + 256, ... of a row, eight
+// loads in flight, and adds in a fixed order.
 __global__ __launch_bounds__(256) void k_is_partials(const float* __restrict__ w, int N, int K,
                                                      const double* __restrict__ d,
                                                      double* __restrict__ part) {
     __shared__ double s1[256], s2[256];
-    const int64_t n = (int64_t)N * K;
     double a = 0.0, b = 0.0;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
-        const double v = (double)w[e] / d[e % K];
-        a += v;
-        b += v * v;
+    const int t = threadIdx.x;
+    for (int n = blockIdx.x; n < N; n += gridDim.x) {
+        const float* wr = w + (int64_t)n * K;
+        int k = t;
+        for (; k + 7 * 256 < K; k += 8 * 256) {
+            float v[8];
+            double dv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                v[u] = wr[k + 256 * u];
+                dv[u] = d[k + 256 * u];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const double x = (double)v[u] / dv[u];
+                a += x;
+                b += x * x;
+            }
+        }
+        for (; k < K; k += 256) {
+            const double x = (double)wr[k] / d[k];
+            a += x;
+            b += x * x;
+        }
     }
-    s1[threadIdx.x] = a;
-    s2[threadIdx.x] = b;
+    s1[t] = a;
+    s2[t] = b;
     __syncthreads();
     for (int m = 128; m >= 1; m >>= 1) {
-        if ((int)threadIdx.x < m) {
-            s1[threadIdx.x] += s1[threadIdx.x + m];
-            s2[threadIdx.x] += s2[threadIdx.x + m];
+        if (t < m) {
+            s1[t] += s1[t + m];
+            s2[t] += s2[t + m];
         }
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
+    if (t == 0) {
         part[2 * blockIdx.x] = s1[0];
         part[2 * blockIdx.x + 1] = s2[0];
     }
@@ -987,9 +1036,8 @@ SA_API int sa_inverse_cholesky_diag(const float* H, int K, double damp, double* 
     double* lambda = reinterpret_cast<double*>(static_cast<char*>(workspace) +
                                                align256((size_t)K * K * sizeof(double)));
     hipLaunchKernelGGL(k_damping, dim3(1), dim3(256), 0, s, H, K, damp, lambda);
-    const int64_t n = (int64_t)K * K;
-    const int grid = (int)(((n + 255) / 256) < 8192 ? (n + 255) / 256 : 8192);
-    hipLaunchKernelGGL(k_reverse, dim3(grid), dim3(256), 0, s, H, K, lambda, A);
+    const int nt = (K + 63) / 64;
+    hipLaunchKernelGGL(k_reverse, dim3(nt * (nt + 1) / 2), dim3(256), 0, s, H, K, lambda, A);
     hipLaunchKernelGGL(k_chol_diag, dim3(1), dim3(256), 0, s, A, K, 0);
     for (int j = 0; j < K; j += kNB) {
         const int below = K - j - kNB;
