@@ -31,6 +31,15 @@ namespace {
 
 // ---------------------------------------------------------------- Gram matrix
 
+// Lower-triangular tile (ti, tj), ti >= tj, of linear block index b.
+__device__ inline void lower_tile(int b, int& ti, int& tj) {
+    int t = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
+    while ((t + 1) * (t + 2) / 2 <= b) ++t;
+    while (t * (t + 1) / 2 > b) --t;
+    ti = t;
+    tj = b - t * (t + 1) / 2;
+}
+
 constexpr int kGT = 128;       // output tile: 128 x 128
 constexpr int kGK = 32;        // calibration columns per stage
 // LDS row stride in halves (80 bytes): 16-byte aligned rows whose 16-byte
@@ -55,12 +64,8 @@ __global__ __launch_bounds__(256) void k_gram_f16(const uint16_t* __restrict__ x
                                                   float* __restrict__ H) {
     __shared__ uint16_t sa[2 * kGBuf];
     __shared__ uint16_t sb[2 * kGBuf];
-    // linear block index -> lower-triangular tile (ti >= tj)
-    const int b = blockIdx.x;
-    int ti = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
-    while ((ti + 1) * (ti + 2) / 2 <= b) ++ti;
-    while (ti * (ti + 1) / 2 > b) --ti;
-    const int tj = b - ti * (ti + 1) / 2;
+    int ti, tj;
+    lower_tile((int)blockIdx.x, ti, tj);
     const int i0 = ti * kGT, j0 = tj * kGT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wi = (wave >> 1) * 64, wj = (wave & 1) * 64;
@@ -459,20 +464,19 @@ __global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ H, int 
 // H[i][j] = H[j][i] for i < j, one lower 64 x 64 tile (or diagonal tile) per workgroup.
 __global__ __launch_bounds__(256) void k_gram_mirror(float* __restrict__ H, int K) {
     __shared__ float t[64][65];
-    const int b = blockIdx.x;
-    int ti = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
-    while ((ti + 1) * (ti + 2) / 2 <= b) ++ti;
-    while (ti * (ti + 1) / 2 > b) --ti;
-    const int tj = b - ti * (ti + 1) / 2;
+    int ti, tj;
+    lower_tile((int)blockIdx.x, ti, tj);
     const int i0 = 64 * ti, j0 = 64 * tj;
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-        const int r = e >> 6, c = e & 63;
-        t[r][c] = H[(int64_t)(i0 + r) * K + j0 + c];
-    }
+    const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
+    float v[16];   // all of a thread's loads in flight before the first LDS write
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = H[(int64_t)(i0 + r0 + 4 * k) * K + j0 + c];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) t[r0 + 4 * k][c] = v[k];
     __syncthreads();
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-        const int r = e >> 6, c = e & 63;
-        const int di = j0 + r, dj = i0 + c;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int r = r0 + 4 * k, di = j0 + r, dj = i0 + c;
         if (di < dj) H[(int64_t)di * K + dj] = t[c][r];
     }
 }
@@ -525,15 +529,6 @@ __global__ __launch_bounds__(256) void k_damping(const float* __restrict__ H, in
         __syncthreads();
     }
     if (threadIdx.x == 0) *lambda = damp * (part[0] / K);
-}
-
-// Lower-triangular tile (ti, tj), ti >= tj, of linear block index b.
-__device__ inline void lower_tile(int b, int& ti, int& tj) {
-    int t = (int)((sqrtf(8.0f * b + 1.0f) - 1.0f) * 0.5f);
-    while ((t + 1) * (t + 2) / 2 <= b) ++t;
-    while (t * (t + 1) / 2 > b) --t;
-    ti = t;
-    tj = b - t * (t + 1) / 2;
 }
 
 // A = J H J + lambda I in fp64 (lower triangle and diagonal), J the reversal:
