@@ -155,6 +155,59 @@ def test_criterion_end_to_end(N, K, T):
     assert C == pytest.approx(ref, rel=1e-4)
 
 
+def test_criterion_full_size():
+    """The criterion at the size `bench.py --criterion` times: N = K = 4096 and
+    262144 calibration tokens (the large-shape Gram path, 64 Cholesky panels),
+    activations drawn as there.  Sampled Gram entries (off-diagonal regions,
+    diagonal regions and their leftover quadrants) against exact fp64 dot
+    products within the Gram bar, the whole matrix symmetric; d for all 4096
+    channels against the oracle from the same fp32 H (relative 1e-9); C, ||IS||
+    and STD(IS) against fp64 statistics of the same d (relative 1e-12)."""
+    N = K = 4096
+    T = 262144
+    say(f"criterion full size N={N} K={K} T={T}: drawing activations")
+    rng = np.random.default_rng(0)
+    x16 = np.empty((K, T), np.float16)
+    out_rows = set(rng.choice(K, K // 100, replace=False).tolist())
+    for r0 in range(0, K, 256):   # row blocks: 4 GB of fp32 draws at once otherwise
+        blk = rng.standard_normal((256, T), dtype=np.float32)
+        for r in range(256):
+            if r0 + r in out_rows:
+                blk[r] *= 20.0
+        x16[r0:r0 + 256] = blk.astype(np.float16)
+    say("  gram")
+    H = gpu_gram(x16)
+    Hn = H.cpu().numpy()
+    assert np.array_equal(Hn, Hn.T)
+    pairs = [(int(i), int(j)) for i, j in zip(rng.integers(0, K, 48), rng.integers(0, K, 48))]
+    for a in rng.integers(0, K // 256, 8):        # inside diagonal 256 x 256 regions
+        base = 256 * int(a)
+        pairs += [(base + int(rng.integers(192, 256)), base + int(rng.integers(128, 256))),
+                  (base + int(rng.integers(0, 256)), base + int(rng.integers(0, 256)))]
+    for i, j in pairs:
+        xi, xj = x16[i].astype(np.float64), x16[j].astype(np.float64)
+        ref = xi @ xj
+        bound = 2 * T * 2.0 ** -24 * (np.abs(xi) @ np.abs(xj))
+        assert abs(float(Hn[i, j]) - ref) <= bound, (i, j, float(Hn[i, j]), ref)
+    del x16
+    say("  inverse cholesky diag")
+    d = gpu_d(H, 0.01)
+    ref_d = alloc.cholesky_diag_of_inverse(alloc.damped(Hn.astype(np.float64), 0.01))
+    assert np.all(np.isfinite(d))
+    assert np.allclose(d, ref_d, rtol=1e-9, atol=0)
+    say("  importance")
+    w = workloads.fp_weights(N, K, seed=1)
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    ws = torch.empty(sa.lib.sa_importance_workspace(), dtype=torch.uint8, device="cuda")
+    sa.sa_importance_criterion(torch.from_numpy(w).cuda(), N, K, torch.from_numpy(d).cuda(), out, ws)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    IS = w.astype(np.float64) / d[None, :]
+    assert o[0] == pytest.approx(np.linalg.norm(IS) * IS.std() ** 2, rel=1e-12)
+    assert o[1] == pytest.approx(np.linalg.norm(IS), rel=1e-12)
+    assert o[2] == pytest.approx(IS.std(), rel=1e-12)
+
+
 def test_allocation_pipeline():
     """Criteria of a few synthetic layers -> per-bit fits against measured
     quantization errors (the GPU quantizer at 2, 3, 4 bits, weighted by the
