@@ -91,7 +91,9 @@ def test_gram_repeatable(K, T):
                                       (1000, 2048, 0.01), (130, 1024, 0.0),
                                       # last diagonal block of 1, 63 and 1 rows; whole panels only
                                       (65, 256, 0.01), (127, 512, 0.01), (129, 512, 0.01),
-                                      (256, 1024, 0.01)])
+                                      (256, 1024, 0.01),
+                                      # one partial diagonal block only
+                                      (1, 32, 0.01), (2, 32, 0.0), (63, 256, 0.01)])
 def test_inverse_cholesky_diag(K, T, damp):
     """Including K not a multiple of the 64-column panel, and no damping on a
     full-rank calibration set."""
